@@ -1,0 +1,11 @@
+"""fp64 CPU oracle (test infrastructure only; see tree_oracle's header).
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  The library never does.
+"""
+from .tree_oracle import (  # noqa: F401
+    GLA, GDN, BF16, F32, MAX_NODES_LIMIT, SUPPORTED_D,
+    OracleError, InvalidArg, BadTree, BadPath, Unsupported,
+    check_problem, check_forest, check_paths, root_path, topology, step,
+    verify, commit, prefix_state,
+)

@@ -1,0 +1,79 @@
+"""The pins must be able to fail: plant plausible mistakes in the oracle's
+update rule (on the CPU) and check that the pin tests reject every one."""
+import numpy as np
+import pytest
+
+import oracle
+import oracle.tree_oracle as to
+from tests import test_oracle_pins as pins
+
+_good_step = to.step
+
+
+def _mut_decay_after_update(mode, St, k, v, g, beta):
+    gamma = np.exp(g)[..., None, None]
+    if mode == to.GLA:
+        return gamma * (St + v[..., :, None] * k[..., None, :])
+    return _good_step(mode, St, k, v, g, beta)
+
+
+def _mut_delta_reads_undecayed(mode, St, k, v, g, beta):
+    if mode == to.GLA:
+        return _good_step(mode, St, k, v, g, beta)
+    gamma = np.exp(g)[..., None, None]
+    u = beta[..., None] * (v - np.einsum("...vk,...k->...v", St, k))
+    return gamma * St + u[..., :, None] * k[..., None, :]
+
+
+def _mut_delta_sign(mode, St, k, v, g, beta):
+    if mode == to.GLA:
+        return _good_step(mode, St, k, v, g, beta)
+    gamma = np.exp(g)[..., None, None]
+    u = beta[..., None] * (v + np.einsum("...vk,...k->...v", gamma * St, k))
+    return gamma * St + u[..., :, None] * k[..., None, :]
+
+
+def _mut_no_beta(mode, St, k, v, g, beta):
+    if mode == to.GLA:
+        return _good_step(mode, St, k, v, g, beta)
+    return _good_step(mode, St, k, v, g, np.ones_like(beta))
+
+
+def _mut_transposed_outer(mode, St, k, v, g, beta):
+    gamma = np.exp(g)[..., None, None]
+    return gamma * St + np.swapaxes(v[..., :, None] * k[..., None, :], -1, -2)
+
+
+def _mut_gate_sign(mode, St, k, v, g, beta):
+    return _good_step(mode, St, k, v, -g, beta)
+
+
+MUTANTS = [_mut_decay_after_update, _mut_delta_reads_undecayed, _mut_delta_sign,
+           _mut_no_beta, _mut_transposed_outer, _mut_gate_sign]
+
+PIN_CHECKS = [
+    pins.test_appendix_scalar_values,
+    lambda: pins.test_chain_equals_token_order_scan(to.GLA),
+    lambda: pins.test_chain_equals_token_order_scan(to.GDN),
+    lambda: pins.test_theorem1_closed_form(to.GLA, 0),
+    lambda: pins.test_theorem1_closed_form(to.GDN, 0),
+    pins.test_delta_rule_with_unit_write_gate_recalls_value,
+]
+
+
+@pytest.mark.parametrize("mutant", MUTANTS, ids=lambda m: m.__name__)
+def test_pins_reject_planted_mistake(mutant, monkeypatch):
+    monkeypatch.setattr(to, "step", mutant)
+    failures = 0
+    for check in PIN_CHECKS:
+        try:
+            check()
+        except (AssertionError, ValueError):
+            failures += 1
+    assert failures > 0, f"no pin caught {mutant.__name__}"
+
+
+def test_pins_pass_unmutated():
+    for check in PIN_CHECKS:
+        check()
+    assert oracle.step is _good_step
