@@ -1,0 +1,153 @@
+/*
+ * treelin — tree-parallel verification and accepted-path commit for recurrent
+ * linear-attention layers (gated linear attention and the gated delta rule)
+ * over a drafted token tree, on AMD Instinct MI355X (gfx950).
+ *
+ * The method follows "Bole: Efficient Tree Speculation for Hybrid-Attention
+ * Language Models" (arXiv 2608.01651):
+ *   - sequential rule and notation: §4.1, Table "Notation for closed-form tree
+ *     verification", restating §2.1 Eq. (gdn-background) node-wise;
+ *   - verify = Theorem 1 of §4.1, Eq. (main-closed-form), built from Lemma 1
+ *     (Eq. path-factorization / factorized-readout) and Lemma 2
+ *     (Eq. correction-system); value tiling as in §4.2 Eq. (kernel-dataflow);
+ *   - commit = §4.4 Eq. (accepted-commit) over the accepted path;
+ *   - forest layout: §5.2 (flat-ragged forest, request offsets + parents).
+ *
+ * Conventions used by every entry point
+ * -------------------------------------
+ * Requests.  A batch of B requests forms a flat-ragged forest.  Request b owns
+ *   global rows node_offsets[b] .. node_offsets[b+1]-1 of every per-node array;
+ *   T_b = node_offsets[b+1] - node_offsets[b] is its node count.
+ * Trees.  parent[r] is request-local: -1 means the node reads the committed
+ *   prefix state S_pre (the paper's pi(i) = 0 with S_0 = S_pre); otherwise
+ *   0 <= parent < the node's own local index (parent-before-child order).
+ *   Several roots per request are allowed.
+ * Heads.  Hk query/key heads, Hv value/state heads (Hv a multiple of Hk);
+ *   v-head h reads q/k head h / (Hv/Hk).
+ * Gates.  g[r, h] is the log-decay (gamma = exp(g), g <= 0 in practice);
+ *   beta[r, h] is the delta rule's write gate.
+ * State.  One slot per request per layer in the canonical [Hv, d_v, d_k]
+ *   layout of §4.4: state[s, h, a, c] is row a (value channel), column c (key
+ *   channel) of the paper's S^T.  A node's output is o = q_scale * S_i^T q_i.
+ *   Gated linear attention:  S_i = gamma_i S_parent + k_i v_i^T.
+ *   Gated delta rule:        u_i = beta_i (v_i - gamma_i S_parent^T k_i),
+ *                            S_i = gamma_i S_parent + k_i u_i^T.
+ * Layouts (all row-major, contiguous, caller-owned DEVICE memory):
+ *   q, k     [N, Hk, d_k]  bf16 or fp32 (tl_problem.in_dtype)
+ *   v        [N, Hv, d_v]  same dtype as q, k
+ *   g, beta  [N, Hv]       fp32
+ *   state    [num_slots, Hv, d_v, d_k] fp32
+ *   out      [N, Hv, d_v]  fp32
+ *   N = node_offsets[B] rows; ints are int32.
+ * Alignment.  q, k, v, state and out must be 16-byte aligned; every other
+ *   pointer 4-byte aligned.
+ * Streams.  `stream` is a hipStream_t (NULL = the null stream).  Every entry
+ *   point only enqueues work on it and returns; results are ready once the
+ *   stream has been synchronised.  The library allocates nothing, keeps no
+ *   global state and is safe to call from several threads.
+ * Errors.  Problems visible from the host (null or misaligned pointers,
+ *   unsupported sizes) return a status synchronously and enqueue nothing.
+ *   Problems only visible in device data are reported through *dev_err (may
+ *   be NULL): the first failing request stores its code there (compare-and-
+ *   swap from 0; the caller zeroes it beforehand) and that request is skipped
+ *   -- verify leaves its output rows unwritten, commit leaves its slot
+ *   untouched.  Other requests are processed normally.
+ */
+#ifndef TREELIN_H
+#define TREELIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TL_OK = 0,
+  TL_EINVAL = 1,       /* bad argument: null/misaligned pointer, bad counts, bad slot */
+  TL_EBADTREE = 2,     /* decreasing node_offsets, T_b > max_nodes, or a bad parent */
+  TL_EBADPATH = 3,     /* accepted path is not a root-first chain of the request's tree */
+  TL_EUNSUPPORTED = 4, /* head dims or max_nodes outside what the kernels implement */
+  TL_EHIP = 5          /* the HIP runtime refused a launch */
+} tl_status;
+
+typedef enum { TL_MODE_GLA = 0, TL_MODE_GDN = 1 } tl_mode;
+typedef enum { TL_BF16 = 0, TL_F32 = 1 } tl_dtype;
+
+typedef struct tl_problem {
+  int32_t batch;        /* B >= 0 requests; 0 is a no-op */
+  int32_t num_qk_heads; /* Hk >= 1 */
+  int32_t num_v_heads;  /* Hv >= 1, a multiple of Hk */
+  int32_t d_k;          /* key channels per head: 16, 32, 64 or 128 */
+  int32_t d_v;          /* value channels per head: equal to d_k */
+  int32_t max_nodes;    /* bound on every T_b, 1..256 (sizes on-chip buffers) */
+  int32_t num_slots;    /* slots in `state`; >= B when `slot` is NULL */
+  int32_t mode;         /* tl_mode */
+  int32_t in_dtype;     /* tl_dtype of q, k, v */
+  float q_scale;        /* multiplies every output (1.0f: none) */
+} tl_problem;
+
+/* Tree-parallel verification (Theorem 1 of §4.1, value-tiled as in §4.2).
+ *
+ * For every node i of every request, writes
+ *   out[i, h, :] = q_scale * S_i^T q_i
+ * where S_i is the state that sequential execution of the recurrence along
+ * the node's root path would produce from S_pre = state[slot(b), h]; no such
+ * per-node state is ever formed.  `beta` must be NULL for TL_MODE_GLA and
+ * non-NULL for TL_MODE_GDN.  `slot` maps request -> state slot ([B] int32,
+ * each in [0, num_slots)); NULL means slot(b) = b.  `state` is only read.
+ * Device errors: TL_EBADTREE (forest), TL_EINVAL (slot index). */
+tl_status tree_lin_attn_verify(const tl_problem* problem,
+                               const int32_t* node_offsets, /* [B+1] */
+                               const int32_t* parent,       /* [N] */
+                               const void* q, const void* k, const void* v,
+                               const float* g, const float* beta,
+                               const float* state, const int32_t* slot,
+                               float* out, int32_t* dev_err, void* stream);
+
+/* Accepted-path commit (§4.4 Eq. accepted-commit).
+ *
+ * For each request b with a non-empty accepted path, overwrites
+ * state[slot(b), h] in place with the post-update state of the path's
+ * terminal node, replaying the path in fp32 from the slot's current
+ * contents.  path_offsets is [B+1] (non-decreasing, path_offsets[0] = 0) and
+ * path[path_offsets[b] .. path_offsets[b+1]-1] lists the accepted nodes,
+ * request-local, root first: path[0] is a root and each later entry is a
+ * child of the one before.  An empty path leaves the slot untouched (no
+ * token accepted keeps S_pre).  Enqueue after the verify that reads the same
+ * slots, on the same stream.  Requests naming the same slot race.
+ * Device errors: TL_EBADTREE (forest), TL_EBADPATH (path), TL_EINVAL (slot,
+ * or decreasing path_offsets). */
+tl_status tree_state_commit(const tl_problem* problem,
+                            const int32_t* node_offsets, const int32_t* parent,
+                            const int32_t* path_offsets, /* [B+1] */
+                            const int32_t* path,         /* [path_offsets[B]] */
+                            const void* k, const void* v,
+                            const float* g, const float* beta,
+                            float* state, const int32_t* slot,
+                            int32_t* dev_err, void* stream);
+
+/* Tree topology of §4.1's notation table, as the kernels build it:
+ * anc_mask[r, w] (W = ceil(max_nodes/64) uint64 words per node) has bit
+ * (j mod 64) of word j/64 set iff local node j is r's node itself or one of
+ * its ancestors (the row of M+ = M- + I); depth[r] is the number of strict
+ * ancestors (a root has depth 0).  Device errors: TL_EBADTREE; rows of a
+ * malformed request are left unwritten. */
+tl_status tree_topology_export(const tl_problem* problem,
+                               const int32_t* node_offsets, const int32_t* parent,
+                               uint64_t* anc_mask, /* [N, W] */
+                               int32_t* depth,     /* [N] */
+                               int32_t* dev_err, void* stream);
+
+/* Static, human-readable name of a status code. */
+const char* tl_status_string(tl_status status);
+
+/* Library version as "major.minor.patch". */
+const char* tl_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TREELIN_H */

@@ -1,0 +1,151 @@
+// C ABI of libtreelin: synchronous argument checks, then one launch on the
+// caller's stream.  Nothing is allocated and no state is kept between calls.
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+#include "tl_kernels.h"
+#include "treelin.h"
+
+namespace {
+
+bool aligned(const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+
+bool supported_d(int d) { return d == 16 || d == 32 || d == 64 || d == 128; }
+
+// Checks shared by every entry point.  Returns TL_OK or the failing status.
+tl_status check_problem(const tl_problem* p) {
+  if (!p) return TL_EINVAL;
+  if (p->batch < 0 || p->num_qk_heads < 1 || p->num_v_heads < 1) return TL_EINVAL;
+  if (p->num_v_heads % p->num_qk_heads) return TL_EINVAL;
+  if (p->mode != TL_MODE_GLA && p->mode != TL_MODE_GDN) return TL_EINVAL;
+  if (p->in_dtype != TL_BF16 && p->in_dtype != TL_F32) return TL_EINVAL;
+  if (!supported_d(p->d_k) || p->d_v != p->d_k) return TL_EUNSUPPORTED;
+  if (p->max_nodes < 1 || p->max_nodes > 256) return TL_EUNSUPPORTED;
+  if (p->batch > 0) {
+    if (p->num_slots < 1) return TL_EINVAL;
+    const long units = (long)p->batch * p->num_v_heads;
+    if (units > (1L << 30)) return TL_EINVAL;
+  }
+  return TL_OK;
+}
+
+tl_status check_tensors(const tl_problem* p, const int32_t* node_offsets, const int32_t* parent,
+                        const void* k, const void* v, const float* g, const float* beta,
+                        const void* state, const int32_t* slot) {
+  if (!node_offsets || !parent || !k || !v || !g || !state) return TL_EINVAL;
+  if ((p->mode == TL_MODE_GLA) != (beta == nullptr)) return TL_EINVAL;
+  if (!aligned(node_offsets, 4) || !aligned(parent, 4) || !aligned(g, 4)) return TL_EINVAL;
+  if (beta && !aligned(beta, 4)) return TL_EINVAL;
+  if (slot && !aligned(slot, 4)) return TL_EINVAL;
+  if (!aligned(k, 16) || !aligned(v, 16) || !aligned(state, 16)) return TL_EINVAL;
+  if (!slot && p->num_slots < p->batch) return TL_EINVAL;
+  return TL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+tl_status tree_lin_attn_verify(const tl_problem* problem, const int32_t* node_offsets,
+                               const int32_t* parent, const void* q, const void* k, const void* v,
+                               const float* g, const float* beta, const float* state,
+                               const int32_t* slot, float* out, int32_t* dev_err, void* stream) {
+  tl_status st = check_problem(problem);
+  if (st != TL_OK) return st;
+  if (problem->batch == 0) return TL_OK;
+  st = check_tensors(problem, node_offsets, parent, k, v, g, beta, state, slot);
+  if (st != TL_OK) return st;
+  if (!q || !out || !aligned(q, 16) || !aligned(out, 16)) return TL_EINVAL;
+  if (dev_err && !aligned(dev_err, 4)) return TL_EINVAL;
+  tl::VerifyArgs a;
+  a.node_offsets = node_offsets;
+  a.parent = parent;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.g = g;
+  a.beta = beta;
+  a.state = state;
+  a.slot = slot;
+  a.out = out;
+  a.dev_err = dev_err;
+  a.batch = problem->batch;
+  a.Hk = problem->num_qk_heads;
+  a.Hv = problem->num_v_heads;
+  a.max_nodes = problem->max_nodes;
+  a.num_slots = problem->num_slots;
+  a.tm = (problem->max_nodes + 15) & ~15;
+  a.q_scale = problem->q_scale;
+  return tl::launch_verify(*problem, a, reinterpret_cast<hipStream_t>(stream));
+}
+
+tl_status tree_state_commit(const tl_problem* problem, const int32_t* node_offsets,
+                            const int32_t* parent, const int32_t* path_offsets, const int32_t* path,
+                            const void* k, const void* v, const float* g, const float* beta,
+                            float* state, const int32_t* slot, int32_t* dev_err, void* stream) {
+  tl_status st = check_problem(problem);
+  if (st != TL_OK) return st;
+  if (problem->batch == 0) return TL_OK;
+  st = check_tensors(problem, node_offsets, parent, k, v, g, beta, state, slot);
+  if (st != TL_OK) return st;
+  if (!path_offsets || !aligned(path_offsets, 4)) return TL_EINVAL;
+  if (path && !aligned(path, 4)) return TL_EINVAL;
+  if (dev_err && !aligned(dev_err, 4)) return TL_EINVAL;
+  tl::CommitArgs a;
+  a.node_offsets = node_offsets;
+  a.parent = parent;
+  a.path_offsets = path_offsets;
+  a.path = path;   // NULL is allowed when every path is empty
+  a.k = k;
+  a.v = v;
+  a.g = g;
+  a.beta = beta;
+  a.state = state;
+  a.slot = slot;
+  a.dev_err = dev_err;
+  a.batch = problem->batch;
+  a.Hk = problem->num_qk_heads;
+  a.Hv = problem->num_v_heads;
+  a.max_nodes = problem->max_nodes;
+  a.num_slots = problem->num_slots;
+  return tl::launch_commit(*problem, a, reinterpret_cast<hipStream_t>(stream));
+}
+
+tl_status tree_topology_export(const tl_problem* problem, const int32_t* node_offsets,
+                               const int32_t* parent, uint64_t* anc_mask, int32_t* depth,
+                               int32_t* dev_err, void* stream) {
+  tl_status st = check_problem(problem);
+  if (st != TL_OK) return st;
+  if (problem->batch == 0) return TL_OK;
+  if (!node_offsets || !parent || !anc_mask || !depth) return TL_EINVAL;
+  if (!aligned(node_offsets, 4) || !aligned(parent, 4) || !aligned(anc_mask, 8) ||
+      !aligned(depth, 4))
+    return TL_EINVAL;
+  if (dev_err && !aligned(dev_err, 4)) return TL_EINVAL;
+  tl::TopoArgs a;
+  a.node_offsets = node_offsets;
+  a.parent = parent;
+  a.anc_mask = anc_mask;
+  a.depth = depth;
+  a.dev_err = dev_err;
+  a.batch = problem->batch;
+  a.max_nodes = problem->max_nodes;
+  a.words = (problem->max_nodes + 63) / 64;
+  return tl::launch_topology(a, reinterpret_cast<hipStream_t>(stream));
+}
+
+const char* tl_status_string(tl_status s) {
+  switch (s) {
+    case TL_OK: return "TL_OK: success";
+    case TL_EINVAL: return "TL_EINVAL: invalid argument";
+    case TL_EBADTREE: return "TL_EBADTREE: malformed forest (offsets or parent array)";
+    case TL_EBADPATH: return "TL_EBADPATH: accepted path is not a root-first chain";
+    case TL_EUNSUPPORTED: return "TL_EUNSUPPORTED: unsupported head dimension or max_nodes";
+    case TL_EHIP: return "TL_EHIP: HIP runtime error";
+  }
+  return "unknown tl_status";
+}
+
+const char* tl_version(void) { return "0.1.0"; }
+
+}  // extern "C"

@@ -1,0 +1,169 @@
+// Device helpers shared by the verify, commit and topology kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "treelin.h"
+
+namespace tl {
+
+constexpr int kThreads = 256;      // every kernel runs 4 wave64s per workgroup
+constexpr int kWaves = kThreads / 64;
+constexpr int kMaxNodes = 256;     // one node per thread in the topology pass
+constexpr int kTile = 16;          // nodes per MFMA tile (M or N of 16x16x32)
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// error reporting: first failing request wins (compare-and-swap from 0)
+// ---------------------------------------------------------------------------
+__device__ inline void report(int32_t* dev_err, int32_t code) {
+  if (dev_err) atomicCAS(dev_err, 0, code);
+}
+
+// ---------------------------------------------------------------------------
+// number formats
+// ---------------------------------------------------------------------------
+__device__ inline float bf2f(__bf16 x) { return (float)x; }
+
+// fp32 -> bf16 hi + bf16 lo with hi + lo == x to about 2^-17 relative
+// (the two-term bf16 split: hi is x rounded to nearest even, lo is the
+// rounded residual).
+__device__ inline void split_bf16(float x, __bf16& hi, __bf16& lo) {
+  hi = (__bf16)x;
+  lo = (__bf16)(x - (float)hi);
+}
+
+// 4 consecutive inputs as floats, from bf16 or fp32 storage.
+template <bool F32IN>
+__device__ inline f32x4 load4(const void* base, size_t idx) {
+  if constexpr (F32IN) {
+    return *reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(base) + idx);
+  } else {
+    bf16x4 t = *reinterpret_cast<const bf16x4*>(reinterpret_cast<const __bf16*>(base) + idx);
+    return f32x4{(float)t[0], (float)t[1], (float)t[2], (float)t[3]};
+  }
+}
+
+template <bool F32IN>
+__device__ inline float load1(const void* base, size_t idx) {
+  if constexpr (F32IN) return reinterpret_cast<const float*>(base)[idx];
+  else return (float)reinterpret_cast<const __bf16*>(base)[idx];
+}
+
+// ---------------------------------------------------------------------------
+// MFMA 16x16x32 bf16 (gfx950).  D = A (16 x 32) * B (32 x 16) + C.
+// Lane l supplies A row (l % 16) and B column (l % 16), each as 8 values of
+// the K range owned by lane group l / 16; D comes back as rows
+// 4*(l/16) .. 4*(l/16)+3 of column (l % 16).
+//
+// The K index is only a contraction index, so any assignment of the 32 K
+// positions to (lane group, element) works as long as A and B use the same
+// one.  Every operand here uses kpos(): group gq holds columns 4gq..4gq+3 and
+// 16+4gq..16+4gq+3 of the 32-wide K chunk, so one 16-byte row load of four
+// lane groups covers 64 contiguous bytes of fp32 state.
+// ---------------------------------------------------------------------------
+__device__ inline int kpos(int gq, int e) { return (e < 4) ? (4 * gq + e) : (16 + 4 * gq + (e - 4)); }
+
+__device__ inline f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Operand fragment (8 bf16) of row `row` (already offset to the row start)
+// for K chunk `ks`, lane group gq: two 8-byte loads.  Returns zeros if !ok.
+__device__ inline bf16x8 frag_bf16(const __bf16* row, int ks, int gq, bool ok) {
+  bf16x8 r;
+  if (ok) {
+    bf16x4 a = *reinterpret_cast<const bf16x4*>(row + ks * 32 + 4 * gq);
+    bf16x4 b = *reinterpret_cast<const bf16x4*>(row + ks * 32 + 16 + 4 * gq);
+    r = bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  } else {
+    __bf16 z = (__bf16)0.0f;
+    r = bf16x8{z, z, z, z, z, z, z, z};
+  }
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// request bounds and forest checks (uniform per workgroup)
+// ---------------------------------------------------------------------------
+struct Request {
+  int off;   // first global row
+  int T;     // node count
+};
+
+// Returns false (and reports TL_EBADTREE) for decreasing offsets or
+// T_b > max_nodes.  Uniform across the block.
+__device__ inline bool load_request(const int32_t* node_offsets, int b, int max_nodes,
+                                    int32_t* dev_err, Request& r) {
+  int o0 = node_offsets[b], o1 = node_offsets[b + 1];
+  r.off = o0;
+  r.T = o1 - o0;
+  if (o0 < 0 || r.T < 0 || r.T > max_nodes) {
+    if (threadIdx.x == 0) report(dev_err, TL_EBADTREE);
+    return false;
+  }
+  return true;
+}
+
+// ---------------------------------------------------------------------------
+// Topology by pointer jumping over the parent array (one thread per node).
+//
+// Computes, for node i = threadIdx.x < T:
+//   depth  = number of strict ancestors,
+//   cl     = sum of x over Anc(i) u {i}   (the cumulative log-decay when x = g,
+//            so P_i = exp(cl_i) and P_i / P_j = exp(cl_i - cl_j)),
+//   mask   = the M+ row of i as W little-endian 64-bit words.
+// After round r every node has folded in the 2^r nodes above it, so the loop
+// ends after ceil(log2(depth + 1)) rounds; all threads take part in every
+// barrier.  Returns false (uniformly) if any parent breaks the
+// parent-before-child order.  Scratch arrays need kThreads entries
+// (kThreads * W words for the mask scratch).
+// ---------------------------------------------------------------------------
+template <int W, bool WANT_MASK>
+__device__ inline bool build_topology(const int32_t* parent_row, int T, float x,
+                                      int32_t* s_jmp, float* s_acc, int32_t* s_cnt,
+                                      uint64_t* s_msk, int& par, int& depth, float& cl,
+                                      uint64_t (&mask)[W]) {
+  const int i = threadIdx.x;
+  par = -1;
+  if (i < T) par = parent_row[i];
+  const bool bad = (i < T) && !(par == -1 || (par >= 0 && par < i));
+  if (__syncthreads_or(bad)) return false;
+
+  int jmp = par;
+  int cnt = 1;
+  cl = x;
+#pragma unroll
+  for (int w = 0; w < W; ++w) mask[w] = 0;
+  if (i < T && WANT_MASK) mask[i >> 6] = 1ull << (i & 63);
+
+  while (__syncthreads_or(i < T && jmp >= 0)) {
+    if (i < T) {
+      s_jmp[i] = jmp;
+      s_acc[i] = cl;
+      s_cnt[i] = cnt;
+      if constexpr (WANT_MASK) {
+#pragma unroll
+        for (int w = 0; w < W; ++w) s_msk[w * kThreads + i] = mask[w];
+      }
+    }
+    __syncthreads();
+    if (i < T && jmp >= 0) {
+      cl += s_acc[jmp];
+      cnt += s_cnt[jmp];
+      if constexpr (WANT_MASK) {
+#pragma unroll
+        for (int w = 0; w < W; ++w) mask[w] |= s_msk[w * kThreads + jmp];
+      }
+      jmp = s_jmp[jmp];
+    }
+  }
+  depth = cnt - 1;
+  return true;
+}
+
+}  // namespace tl

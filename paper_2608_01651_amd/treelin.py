@@ -1,0 +1,153 @@
+"""ctypes binding of libtreelin (argument marshalling only).
+
+Every function takes torch tensors that already live on the GPU, passes their
+device pointers and torch's current HIP stream to the C ABI declared in
+include/treelin.h, and returns immediately (the work is asynchronous on that
+stream).  A non-OK synchronous status raises TreeLinError.  The library must
+have been built (python -m paper_2608_01651_amd.build); nothing here falls
+back to another implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtreelin.so")
+
+TL_OK, TL_EINVAL, TL_EBADTREE, TL_EBADPATH, TL_EUNSUPPORTED, TL_EHIP = range(6)
+GLA, GDN = 0, 1
+BF16, F32 = 0, 1
+
+
+class TreeLinError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)}")
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("num_qk_heads", ctypes.c_int32),
+        ("num_v_heads", ctypes.c_int32),
+        ("d_k", ctypes.c_int32),
+        ("d_v", ctypes.c_int32),
+        ("max_nodes", ctypes.c_int32),
+        ("num_slots", ctypes.c_int32),
+        ("mode", ctypes.c_int32),
+        ("in_dtype", ctypes.c_int32),
+        ("q_scale", ctypes.c_float),
+    ]
+
+
+def problem(batch, num_qk_heads, num_v_heads, d_k, d_v, max_nodes, num_slots=None,
+            mode=GLA, in_dtype=BF16, q_scale=1.0):
+    return Problem(batch, num_qk_heads, num_v_heads, d_k, d_v, max_nodes,
+                   batch if num_slots is None else num_slots, mode, in_dtype, q_scale)
+
+
+_lib = None
+
+
+def lib():
+    """The loaded shared library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                               "`python -m paper_2608_01651_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.POINTER(Problem)
+        vp = ctypes.c_void_p
+        L.tree_lin_attn_verify.argtypes = [P] + [vp] * 12
+        L.tree_lin_attn_verify.restype = ctypes.c_int
+        L.tree_state_commit.argtypes = [P] + [vp] * 12
+        L.tree_state_commit.restype = ctypes.c_int
+        L.tree_topology_export.argtypes = [P] + [vp] * 6
+        L.tree_topology_export.restype = ctypes.c_int
+        L.tl_status_string.argtypes = [ctypes.c_int]
+        L.tl_status_string.restype = ctypes.c_char_p
+        L.tl_version.argtypes = []
+        L.tl_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def status_string(status):
+    return lib().tl_status_string(int(status)).decode()
+
+
+def version():
+    return lib().tl_version().decode()
+
+
+_DT = {torch.int32: "int32", torch.float32: "float32", torch.bfloat16: "bfloat16",
+       torch.int64: "int64"}
+
+
+def _ptr(t, name, dtypes, optional=False):
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if isinstance(t, int):
+        return t
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr() or None
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+_IN = (torch.bfloat16, torch.float32)
+_I32 = (torch.int32,)
+_F32 = (torch.float32,)
+
+
+def _check(status, where):
+    if status != TL_OK:
+        raise TreeLinError(status, where)
+
+
+def verify(prob, node_offsets, parent, q, k, v, g, beta, state, out, slot=None,
+           dev_err=None, stream=None):
+    """tree_lin_attn_verify: writes out [N, Hv, d_v] fp32."""
+    s = lib().tree_lin_attn_verify(
+        ctypes.byref(prob), _ptr(node_offsets, "node_offsets", _I32), _ptr(parent, "parent", _I32),
+        _ptr(q, "q", _IN), _ptr(k, "k", _IN), _ptr(v, "v", _IN), _ptr(g, "g", _F32),
+        _ptr(beta, "beta", _F32, True), _ptr(state, "state", _F32), _ptr(slot, "slot", _I32, True),
+        _ptr(out, "out", _F32), _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
+    _check(s, "tree_lin_attn_verify")
+
+
+def commit(prob, node_offsets, parent, path_offsets, path, k, v, g, beta, state, slot=None,
+           dev_err=None, stream=None):
+    """tree_state_commit: overwrites the slots of requests with a non-empty path."""
+    s = lib().tree_state_commit(
+        ctypes.byref(prob), _ptr(node_offsets, "node_offsets", _I32), _ptr(parent, "parent", _I32),
+        _ptr(path_offsets, "path_offsets", _I32), _ptr(path, "path", _I32, True),
+        _ptr(k, "k", _IN), _ptr(v, "v", _IN), _ptr(g, "g", _F32), _ptr(beta, "beta", _F32, True),
+        _ptr(state, "state", _F32), _ptr(slot, "slot", _I32, True),
+        _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
+    _check(s, "tree_state_commit")
+
+
+def topology(prob, node_offsets, parent, anc_mask, depth, dev_err=None, stream=None):
+    """tree_topology_export: M+ rows [N, ceil(max_nodes/64)] (int64 bit patterns) and depths."""
+    s = lib().tree_topology_export(
+        ctypes.byref(prob), _ptr(node_offsets, "node_offsets", _I32), _ptr(parent, "parent", _I32),
+        _ptr(anc_mask, "anc_mask", (torch.int64,)), _ptr(depth, "depth", _I32),
+        _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
+    _check(s, "tree_topology_export")
