@@ -1,0 +1,348 @@
+"""Benchmark: verified tree-tokens/s per linear-attention layer on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload production]
+
+One step is one pass of the hot path over one batch: tree-parallel verify of
+one layer's draft forest, then the accepted-path commit of that layer's state.
+The timed loop keeps R independent layer buffer sets resident in HBM (R chosen
+so the sets exceed twice the 256 MB Infinity Cache) and runs, per round,
+verify over all R layers and then commit over the same R layers -- the order
+of a real forward pass, where every layer verifies before sampling and the
+commit follows.  Inputs are resident before timing starts; the step count is
+rounded up to a multiple of R.
+
+The JSON line reports whole-job throughput (tree tokens / s per layer), the
+HIP-event average duration of each kernel, the algorithmic HBM bytes each
+kernel must move, the roofline of the dominant kernel against the MI355X's
+8 TB/s, and the fp64 oracle timed on host cores over a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MALL_BYTES = 256 << 20
+METRIC = "verified tree-tokens/s per linear-attn layer; % of HBM roofline (1 MI355X)"
+
+
+# ---------------------------------------------------------------------------
+# algorithmic bytes (what the method must move; no per-node state traffic)
+# ---------------------------------------------------------------------------
+def verify_bytes(cfg, N, B):
+    Q = 4 if cfg.in_dtype == "f32" else 2
+    gdn = 1 if cfg.mode == 1 else 0
+    Hk, Hv, dk, dv = cfg.num_qk_heads, cfg.num_v_heads, cfg.d_k, cfg.d_v
+    per_node = 2 * Hk * dk * Q + Hv * dv * Q + Hv * 4 * (1 + gdn) + 4
+    return N * per_node + 4 * (B + 1) + B * Hv * dk * dv * 4 + N * Hv * dv * 4
+
+
+def commit_bytes(cfg, path_lens):
+    Q = 4 if cfg.in_dtype == "f32" else 2
+    gdn = 1 if cfg.mode == 1 else 0
+    Hk, Hv, dk, dv = cfg.num_qk_heads, cfg.num_v_heads, cfg.d_k, cfg.d_v
+    L = np.asarray(path_lens)
+    per_row = Hk * dk * Q + Hv * dv * Q + Hv * 4 * (1 + gdn) + 4
+    return int((L > 0).sum()) * 2 * Hv * dk * dv * 4 + int(L.sum()) * per_row + 4 * (L.size + 1)
+
+
+def source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_01651_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+# ---------------------------------------------------------------------------
+# GPU leg
+# ---------------------------------------------------------------------------
+class LayerSet:
+    """One layer's resident inputs: the forest, q/k/v/gates and its state slots."""
+
+    def __init__(self, w, state_t, torch):
+        from synth.upload import Uploaded
+        self.up = Uploaded(w)
+        self.state = state_t
+        self.out = torch.empty((w.N, w.cfg.num_v_heads, w.cfg.d_v), dtype=torch.float32,
+                               device=state_t.device)
+
+
+def build_prefix_state_gpu(cfg, seed, batch, torch, tl, log):
+    """S_pre of every request: the library's own commit replays each request's
+    synthetic prefix (chunks of 256 tokens as chain trees) from a zero state."""
+    from synth import workloads as W
+    dev = torch.device("cuda:0")
+    state = torch.zeros((batch, cfg.num_v_heads, cfg.d_v, cfg.d_k), dtype=torch.float32, device=dev)
+    prob = tl.problem(batch, cfg.num_qk_heads, cfg.num_v_heads, cfg.d_k, cfg.d_v, W.PREFIX_CHUNK,
+                      mode=cfg.mode, in_dtype=tl.F32 if cfg.in_dtype == "f32" else tl.BF16)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    in_t = torch.float32 if cfg.in_dtype == "f32" else torch.bfloat16
+    for c in range(W.prefix_chunks(cfg)):
+        parts = [W.prefix_chunk(cfg, seed, b, c) for b in range(batch)]
+        L = parts[0][0].shape[0]
+        offs = torch.arange(0, (batch + 1) * L, L, dtype=torch.int32, device=dev)
+        parent = torch.arange(-1, L - 1, dtype=torch.int32, device=dev).repeat(batch)
+        path = torch.arange(0, L, dtype=torch.int32, device=dev).repeat(batch)
+        k = torch.from_numpy(np.concatenate([p[0] for p in parts])).to(dev).to(in_t)
+        v = torch.from_numpy(np.concatenate([p[1] for p in parts])).to(dev).to(in_t)
+        g = torch.from_numpy(np.concatenate([p[2] for p in parts])).to(dev)
+        beta = None if parts[0][3] is None else torch.from_numpy(np.concatenate([p[3] for p in parts])).to(dev)
+        tl.commit(prob, offs, parent, offs, path, k, v, g, beta, state, dev_err=err)
+    torch.cuda.synchronize()
+    if err.item() != 0:
+        raise RuntimeError(f"prefix commit reported {tl.status_string(err.item())}")
+    log(f"prefix state built from {cfg.prefix_len} tokens per request")
+    return state
+
+
+def gpu_leg(args, cfg, log):
+    import torch
+    from paper_2608_01651_amd import treelin as tl
+    from synth import workloads as W
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU (HIP) device")
+    tl.lib()   # fail loudly if the library is missing
+    w = W.make(cfg, seed=args.seed)
+    log(f"workload {cfg.name}: B={w.batch} N={w.N} paths={int(w.path.size)} rows")
+    if cfg.prefix_len:
+        state0 = build_prefix_state_gpu(cfg, args.seed, w.batch, torch, tl, log)
+    else:
+        state0 = torch.from_numpy(w.state).to("cuda:0")
+    vb = verify_bytes(cfg, w.N, w.batch)
+    cb = commit_bytes(cfg, np.diff(w.path_offsets))
+    # a layer set's footprint is what verify touches: state, q/k/v/gates, output
+    R = args.layers or max(1, math.ceil(2 * MALL_BYTES / vb))
+    sets = []
+    for r in range(R):
+        sets.append(LayerSet(w, state0.clone(), torch))
+    log(f"{R} layer sets resident ({R * vb / 1e6:.0f} MB of verify footprint)")
+    prob = tl.problem(w.batch, cfg.num_qk_heads, cfg.num_v_heads, cfg.d_k, cfg.d_v, cfg.max_nodes,
+                      mode=cfg.mode, in_dtype=tl.F32 if cfg.in_dtype == "f32" else tl.BF16,
+                      q_scale=cfg.q_scale)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda:0")
+    stream = torch.cuda.current_stream()
+
+    def run_verify(s):
+        u = s.up
+        tl.verify(prob, u.node_offsets, u.parent, u.q, u.k, u.v, u.g, u.beta, s.state, s.out,
+                  dev_err=err)
+
+    def run_commit(s):
+        u = s.up
+        tl.commit(prob, u.node_offsets, u.parent, u.path_offsets, u.path, u.k, u.v, u.g, u.beta,
+                  s.state, dev_err=err)
+
+    rounds_w = max(1, math.ceil(args.warmup / R))
+    for _ in range(rounds_w):
+        for s in sets:
+            run_verify(s)
+        for s in sets:
+            run_commit(s)
+    torch.cuda.synchronize()
+    if err.item() != 0:
+        raise RuntimeError(f"device error {tl.status_string(err.item())}")
+
+    rounds = max(1, math.ceil(args.steps / R))
+    steps = rounds * R
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(rounds)]
+    torch.cuda.synchronize()
+    t_host0 = time.perf_counter()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for r in range(rounds):
+        ev[r][0].record(stream)
+        for s in sets:
+            run_verify(s)
+        ev[r][1].record(stream)
+        for s in sets:
+            run_commit(s)
+        ev[r][2].record(stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_host0
+    if err.item() != 0:
+        raise RuntimeError(f"device error {tl.status_string(err.item())}")
+    total_ms = start.elapsed_time(end)
+    v_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / (rounds * R)
+    c_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / (rounds * R)
+    log(f"timed {steps} steps: {total_ms:.3f} ms (host wall {wall * 1e3:.1f} ms); "
+        f"verify {v_ms * 1e3:.2f} us, commit {c_ms * 1e3:.2f} us per launch")
+    return dict(w=w, steps=steps, R=R, total_ms=total_ms, verify_ms=v_ms, commit_ms=c_ms,
+                verify_bytes=vb, commit_bytes=cb)
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the fp64 oracle on a bounded sample of the same workload
+# ---------------------------------------------------------------------------
+_CPU_CTX = {}
+
+
+def _cpu_init():
+    try:
+        from threadpoolctl import threadpool_limits
+        threadpool_limits(1)
+    except Exception:
+        pass
+
+
+def _cpu_prefix(args):
+    """S_pre of request b from the oracle's recurrence over its prefix."""
+    cfg_name, seed, b = args
+    import oracle
+    from synth import workloads as W
+    cfg = W.CONFIGS[cfg_name]
+    if not cfg.prefix_len:
+        return W.make(cfg, seed=seed, requests=[b]).state
+    grp = cfg.num_v_heads // cfg.num_qk_heads
+    St = None
+    for c in range(W.prefix_chunks(cfg)):
+        k, v, g, beta = W.prefix_chunk(cfg, seed, b, c)
+        St = oracle.prefix_state(cfg.mode, k[:, np.arange(cfg.num_v_heads) // grp], v, g, beta, St0=St)
+    return St[None].astype(np.float32)
+
+
+def _cpu_request(args):
+    cfg_name, seed, b, state = args
+    import oracle
+    from synth import workloads as W
+    cfg = W.CONFIGS[cfg_name]
+    w = W.make(cfg, seed=seed, requests=[b])
+    oracle.verify(cfg.mode, cfg.num_qk_heads, w.node_offsets, w.parent, w.q, w.k, w.v, w.g,
+                  w.beta, state, q_scale=cfg.q_scale, max_nodes=cfg.max_nodes)
+    oracle.commit(cfg.mode, cfg.num_qk_heads, w.node_offsets, w.parent, w.path_offsets, w.path,
+                  w.k, w.v, w.g, w.beta, state, max_nodes=cfg.max_nodes)
+    return w.N
+
+
+def cpu_baseline(args, cfg, log):
+    import concurrent.futures as cf
+    import multiprocessing as mp
+    from synth import workloads as W
+    cores = len(os.sched_getaffinity(0))
+    cores = max(1, min(cores, 16, cfg.batch))
+    nreq = min(cfg.batch, max(cores, args.cpu_requests))
+    reqs = list(range(nreq))
+    ctx = mp.get_context("fork")
+    with cf.ProcessPoolExecutor(max_workers=cores, mp_context=ctx, initializer=_cpu_init) as ex:
+        states = list(ex.map(_cpu_prefix, [(cfg.name, args.seed, b) for b in reqs]))
+        # the timed region covers drawing each request's tree inputs (cheap)
+        # and the oracle's verify + commit of it
+        t0 = time.perf_counter()
+        nodes = sum(ex.map(_cpu_request, [(cfg.name, args.seed, b, s) for b, s in zip(reqs, states)]))
+        dt = time.perf_counter() - t0
+    log(f"oracle: {nodes} nodes of {nreq} requests in {dt:.2f} s on {cores} processes")
+    cpu_model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": nodes / dt, "unit": "tree-tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"fp64 oracle verify+commit of requests 0..{nreq - 1} of the {cfg.name} "
+                      f"workload ({nodes} tree nodes), one process per core, "
+                      f"{dt:.2f} s wall; CPU: {cpu_model}"}
+
+
+def traffic_for(cfg_name, kernel):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they
+    were taken on the current kernel sources."""
+    p = os.path.join(ROOT, "profiles", f"traffic_{cfg_name}.json")
+    try:
+        d = json.load(open(p))
+    except (OSError, ValueError):
+        return None
+    if d.get("src_hash") != source_hash() or kernel not in d:
+        return None
+    return d[kernel].get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=40)
+    ap.add_argument("--workload", default="production",
+                    choices=["tiny", "mid", "production", "gdn", "large"])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--layers", type=int, default=0, help="layer buffer sets (0: auto)")
+    ap.add_argument("--cpu-requests", type=int, default=16)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--quiet", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(every (request, head) unit is independent; see the design notes on sharding).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    def log(msg):
+        if not args.quiet:
+            print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    from synth import workloads as W
+    cfg = W.CONFIGS[args.workload]
+    cpu = None
+    if not args.no_cpu_baseline:
+        # before the GPU is touched, so the worker pool may fork
+        cpu = cpu_baseline(args, cfg, log)
+    g = gpu_leg(args, cfg, log)
+    w = g["w"]
+    ms_step = g["total_ms"] / g["steps"]
+    value = w.N / (ms_step * 1e-3)
+    path_frac = (g["verify_bytes"] + g["commit_bytes"]) / (ms_step * 1e-3) / (HBM_PEAK_GBS * 1e9)
+    kern = {"verify": (g["verify_ms"], g["verify_bytes"]), "commit": (g["commit_ms"], g["commit_bytes"])}
+    dom = max(kern, key=lambda k: kern[k][0])
+    dom_ms, dom_bytes = kern[dom]
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic_for(cfg.name, dom),
+                "algorithmic_bytes_per_launch": int(dom_bytes)}
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tree-tokens/s",
+        "n_gpus": 1,
+        "steps": g["steps"],
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{cfg.name}: B={w.batch}, Hk={cfg.num_qk_heads}, Hv={cfg.num_v_heads}, "
+                        f"d_k=d_v={cfg.d_k}, {'gated delta rule' if cfg.mode else 'gated linear attention'}, "
+                        f"{w.N} tree nodes, {cfg.in_dtype} q/k/v, fp32 state and output",
+            "batch": w.batch, "tree_nodes": w.N, "accepted_rows": int(w.path.size),
+            "in_dtype": cfg.in_dtype, "layer_sets": g["R"], "parallelism": "none (1 GPU)",
+        },
+        "verify_us": round(g["verify_ms"] * 1e3, 3),
+        "commit_us": round(g["commit_ms"] * 1e3, 3),
+        "path_hbm_frac": round(path_frac, 4),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -49,6 +49,18 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
     if (tid == 0) report(a.dev_err, TL_EINVAL);
     return;
   }
+  // the slot is read first (whole tile into registers) so that its latency
+  // overlaps the checks below; nothing is written before they pass
+  float* Sp = a.state + ((size_t)sidx * a.Hv + h) * D * D;
+  const int col = (tid % LPR) * 4;
+  f32x4 st[PASSES];
+  if (Lp > 0) {
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int row = p * RPP + tid / LPR;
+      if (row < D) st[p] = *reinterpret_cast<const f32x4*>(Sp + (size_t)row * D + col);
+    }
+  }
   // forest of request b (one node per thread)
   {
     bool bad = false;
@@ -75,15 +87,6 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
     }
   }
   if (Lp == 0) return;
-
-  float* Sp = a.state + ((size_t)sidx * a.Hv + h) * D * D;
-  const int col = (tid % LPR) * 4;
-  f32x4 st[PASSES];
-#pragma unroll
-  for (int p = 0; p < PASSES; ++p) {
-    const int row = p * RPP + tid / LPR;
-    if (row < D) st[p] = *reinterpret_cast<const f32x4*>(Sp + (size_t)row * D + col);
-  }
 
   const size_t qk_row = (size_t)a.Hk * D, v_row = (size_t)a.Hv * D;
   for (int c0 = 0; c0 < Lp; c0 += kCommitChunk) {

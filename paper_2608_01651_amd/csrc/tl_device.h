@@ -112,6 +112,7 @@ __device__ inline bool load_request(const int32_t* node_offsets, int b, int max_
 // ---------------------------------------------------------------------------
 // Topology by pointer jumping over the parent array (one thread per node).
 //
+// `par` is node i's parent (any value for threads i >= T).
 // Computes, for node i = threadIdx.x < T:
 //   depth  = number of strict ancestors,
 //   cl     = sum of x over Anc(i) u {i}   (the cumulative log-decay when x = g,
@@ -124,13 +125,11 @@ __device__ inline bool load_request(const int32_t* node_offsets, int b, int max_
 // (kThreads * W words for the mask scratch).
 // ---------------------------------------------------------------------------
 template <int W, bool WANT_MASK>
-__device__ inline bool build_topology(const int32_t* parent_row, int T, float x,
+__device__ inline bool build_topology(int par, int T, float x,
                                       int32_t* s_jmp, float* s_acc, int32_t* s_cnt,
-                                      uint64_t* s_msk, int& par, int& depth, float& cl,
+                                      uint64_t* s_msk, int& depth, float& cl,
                                       uint64_t (&mask)[W]) {
   const int i = threadIdx.x;
-  par = -1;
-  if (i < T) par = parent_row[i];
   const bool bad = (i < T) && !(par == -1 || (par >= 0 && par < i));
   if (__syncthreads_or(bad)) return false;
 
@@ -138,8 +137,7 @@ __device__ inline bool build_topology(const int32_t* parent_row, int T, float x,
   int cnt = 1;
   cl = x;
 #pragma unroll
-  for (int w = 0; w < W; ++w) mask[w] = 0;
-  if (i < T && WANT_MASK) mask[i >> 6] = 1ull << (i & 63);
+  for (int w = 0; w < W; ++w) mask[w] = (i < T && WANT_MASK && (i >> 6) == w) ? (1ull << (i & 63)) : 0ull;
 
   while (__syncthreads_or(i < T && jmp >= 0)) {
     if (i < T) {
@@ -164,6 +162,65 @@ __device__ inline bool build_topology(const int32_t* parent_row, int T, float x,
   }
   depth = cnt - 1;
   return true;
+}
+
+}  // namespace tl
+
+namespace tl {
+
+// Number of set bits of the W-word mask m strictly below bit j.
+template <int W>
+__device__ inline int popc_below(const uint64_t (&m)[W], int j) {
+  int c = 0;
+#pragma unroll
+  for (int w = 0; w < W; ++w) {
+    if (64 * w + 64 <= j) c += __popcll(m[w]);
+    else if (64 * w <= j) c += __popcll(m[w] & ((1ull << (j - 64 * w)) - 1ull));
+  }
+  return c;
+}
+
+// ---------------------------------------------------------------------------
+// Direct global -> LDS copies (gfx950 global_load_lds_dwordx4): each lane's
+// 16 bytes land at lds_base + 16 * lane, without passing through registers.
+// `lds_base` must be the same for the whole wave.
+// ---------------------------------------------------------------------------
+__device__ inline void copy16_to_lds(const void* gsrc, void* lds_base) {
+  __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+
+// Waits for every outstanding vector memory operation of this wave
+// (including the direct-to-LDS copies).
+__device__ inline void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Rows of CPR 16-byte chunks are stored with chunk c at position
+// c ^ (row & (CPR-1)) so that the same column of 16 consecutive rows falls in
+// different LDS banks.
+template <int CPR>
+__device__ inline int swz(int row, int chunk) { return chunk ^ (row & (CPR - 1)); }
+
+// Stage rows [0, T) of a strided bf16 matrix (row r at src + r * stride,
+// CPR chunks of 8 values each) into swizzled LDS.  All threads of the block
+// take part; completion needs wait_vmem() and a barrier.
+template <int CPR>
+__device__ inline void stage_rows_bf16(const __bf16* src, size_t stride, int T, __bf16* lds) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int total = T * CPR;
+  for (int base = wave * 64; base < total; base += kThreads) {
+    const int p = base + lane;
+    if (p < total) {
+      const int r = p / CPR, c = swz<CPR>(r, p % CPR);
+      copy16_to_lds(src + (size_t)r * stride + c * 8, lds + (size_t)base * 8);
+    }
+  }
+}
+
+// 4 bf16 (8 bytes) at logical column `col` (multiple of 4) of row `row` of a
+// swizzled LDS matrix.
+template <int CPR>
+__device__ inline bf16x4 lds_bf16x4(const __bf16* lds, int row, int col) {
+  const int c = swz<CPR>(row, col >> 3);
+  return *reinterpret_cast<const bf16x4*>(lds + ((size_t)row * CPR + c) * 8 + (col & 7));
 }
 
 }  // namespace tl

@@ -18,11 +18,11 @@ __global__ __launch_bounds__(kThreads) void topology_kernel(TopoArgs a) {
   Request rq;
   if (!load_request(a.node_offsets, blockIdx.x, a.max_nodes, a.dev_err, rq)) return;
   if (rq.T == 0) return;
-  int par, dep;
+  int dep;
   float cl;
   uint64_t msk[4];
-  if (!build_topology<4, true>(a.parent + rq.off, rq.T, 0.f, s_jmp, s_acc, s_cnt, s_msk, par, dep,
-                               cl, msk)) {
+  const int par = (tid < rq.T) ? a.parent[rq.off + tid] : -1;
+  if (!build_topology<4, true>(par, rq.T, 0.f, s_jmp, s_acc, s_cnt, s_msk, dep, cl, msk)) {
     if (tid == 0) report(a.dev_err, TL_EBADTREE);
     return;
   }

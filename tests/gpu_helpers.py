@@ -12,21 +12,11 @@ from synth import workloads as W
 TOL = 2e-3   # max relative error on outputs and committed states
 
 
+from synth.upload import Uploaded, t_f32, t_in, t_int  # noqa: F401
+
+
 def dev():
     return torch.device("cuda:0")
-
-
-def t_int(x):
-    return torch.from_numpy(np.ascontiguousarray(np.asarray(x, dtype=np.int32))).to(dev())
-
-
-def t_f32(x):
-    return torch.from_numpy(np.ascontiguousarray(np.asarray(x, dtype=np.float32))).to(dev())
-
-
-def t_in(x, in_dtype):
-    t = t_f32(x)
-    return t if in_dtype == "f32" else t.to(torch.bfloat16)   # values are bf16-exact already
 
 
 def oracle_prefix_state(cfg, seed, requests):
@@ -49,21 +39,6 @@ def problem_for(cfg, batch, num_slots=None):
     return tl.problem(batch, cfg.num_qk_heads, cfg.num_v_heads, cfg.d_k, cfg.d_v, cfg.max_nodes,
                       num_slots=num_slots, mode=cfg.mode,
                       in_dtype=tl.F32 if cfg.in_dtype == "f32" else tl.BF16, q_scale=cfg.q_scale)
-
-
-class Uploaded:
-    def __init__(self, w: W.Workload):
-        cfg = w.cfg
-        self.w = w
-        self.node_offsets = t_int(w.node_offsets)
-        self.parent = t_int(w.parent) if w.N else torch.zeros(1, dtype=torch.int32, device=dev())
-        self.q = t_in(w.q, cfg.in_dtype)
-        self.k = t_in(w.k, cfg.in_dtype)
-        self.v = t_in(w.v, cfg.in_dtype)
-        self.g = t_f32(w.g)
-        self.beta = None if w.beta is None else t_f32(w.beta)
-        self.path_offsets = t_int(w.path_offsets)
-        self.path = t_int(w.path) if w.path.size else None
 
 
 def run_verify(cfg, up: Uploaded, state_t, slot=None, num_slots=None, max_nodes=None):
