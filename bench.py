@@ -260,6 +260,31 @@ def cpu_baseline(args, cfg, log):
                       f"{dt:.2f} s wall; CPU: {cpu_model}"}
 
 
+def calibrate_copy(log):
+    """A plain device-to-device copy of 512 MiB (torch copy_), the reference
+    kernel for scaling rocprofv3's FETCH_SIZE / WRITE_SIZE and the achievable
+    copy bandwidth (read + write bytes / time)."""
+    import torch
+    n = (512 << 20) // 4
+    src = torch.empty(n, dtype=torch.float32, device="cuda:0").uniform_()
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 10
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    gbs = 2 * src.numel() * 4 / (ms * 1e-3) / 1e9
+    log(f"copy of {src.numel() * 4 >> 20} MiB: {ms * 1e3:.1f} us, {gbs:.0f} GB/s read+write")
+    print(json.dumps({"copy_bytes": src.numel() * 4, "copy_us": round(ms * 1e3, 2),
+                      "copy_gbs": round(gbs, 1)}), flush=True)
+
+
 def traffic_for(cfg_name, kernel):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they
     were taken on the current kernel sources."""
@@ -285,6 +310,8 @@ def main():
     ap.add_argument("--cpu-requests", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quiet", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only time a plain 512 MiB device copy (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -296,6 +323,9 @@ def main():
         if not args.quiet:
             print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
+    if args.calibrate_copy:
+        calibrate_copy(log)
+        return
     from synth import workloads as W
     cfg = W.CONFIGS[args.workload]
     cpu = None

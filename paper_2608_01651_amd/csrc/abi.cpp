@@ -8,6 +8,10 @@
 
 namespace {
 
+#ifdef TL_TRACE
+long long* g_trace = nullptr;
+#endif
+
 bool aligned(const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
 
 bool supported_d(int d) { return d == 16 || d == 32 || d == 64 || d == 128; }
@@ -46,6 +50,11 @@ tl_status check_tensors(const tl_problem* p, const int32_t* node_offsets, const 
 
 extern "C" {
 
+#ifdef TL_TRACE
+// Trace builds only: stamps of the next verify launches go to p ([blocks][16]).
+void tl_set_trace(long long* p) { g_trace = p; }
+#endif
+
 tl_status tree_lin_attn_verify(const tl_problem* problem, const int32_t* node_offsets,
                                const int32_t* parent, const void* q, const void* k, const void* v,
                                const float* g, const float* beta, const float* state,
@@ -76,6 +85,9 @@ tl_status tree_lin_attn_verify(const tl_problem* problem, const int32_t* node_of
   a.num_slots = problem->num_slots;
   a.tm = (problem->max_nodes + 15) & ~15;
   a.q_scale = problem->q_scale;
+#ifdef TL_TRACE
+  a.trace = g_trace;
+#endif
   return tl::launch_verify(*problem, a, reinterpret_cast<hipStream_t>(stream));
 }
 

@@ -6,6 +6,20 @@
 
 #include "treelin.h"
 
+// Phase time stamps for trace builds (-DTL_TRACE): thread 0 of each block
+// records the 100 MHz wall clock at point k.  Empty in normal builds.
+#ifdef TL_TRACE
+#define TL_TRACE_POINT(args, k)                                                           \
+  do {                                                                                    \
+    if ((args).trace && threadIdx.x == 0)                                                 \
+      (args).trace[(size_t)blockIdx.x * 16 + (k)] = wall_clock64();                       \
+  } while (0)
+#else
+#define TL_TRACE_POINT(args, k) \
+  do {                          \
+  } while (0)
+#endif
+
 namespace tl {
 
 constexpr int kThreads = 256;      // every kernel runs 4 wave64s per workgroup
@@ -221,6 +235,59 @@ template <int CPR>
 __device__ inline bf16x4 lds_bf16x4(const __bf16* lds, int row, int col) {
   const int c = swz<CPR>(row, col >> 3);
   return *reinterpret_cast<const bf16x4*>(lds + ((size_t)row * CPR + c) * 8 + (col & 7));
+}
+
+// MFMA operand fragment (kpos() layout) of row `row`, K chunk ks, lane group
+// gq, from a swizzled LDS matrix; zeros if !ok.
+template <int CPR>
+__device__ inline bf16x8 lds_frag(const __bf16* lds, int row, int ks, int gq, bool ok) {
+  const bf16x4 x0 = lds_bf16x4<CPR>(lds, row, ks * 32 + 4 * gq);
+  const bf16x4 x1 = lds_bf16x4<CPR>(lds, row, ks * 32 + 16 + 4 * gq);
+  return ok ? bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]} : bf16x8{};
+}
+
+}  // namespace tl
+
+namespace tl {
+
+// 64-bit lane shuffle (two 32-bit ds_bpermute).
+__device__ inline uint64_t shfl64(uint64_t x, int src) {
+  const unsigned lo = __shfl((unsigned)(x & 0xffffffffull), src, 64);
+  const unsigned hi = __shfl((unsigned)(x >> 32), src, 64);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Topology of a tree of T <= 64 nodes inside one wavefront, lane = node,
+// by pointer jumping over lane shuffles (no LDS, no barriers).  `par` is the
+// lane's parent (ignored for lanes >= T).  Returns false (for the whole
+// wave) if a parent breaks the parent-before-child order; otherwise gives
+// the lane's depth, its sum of x along the root path (inclusive) and its M+
+// row as one 64-bit word.
+__device__ inline bool wave_topology(int par, int T, float x, int& depth, float& cl,
+                                     uint64_t& mask) {
+  const int i = threadIdx.x & 63;
+  const bool live = i < T;
+  const bool bad = live && !(par == -1 || (par >= 0 && par < i));
+  if (__ballot(bad)) return false;
+  int jmp = live ? par : -1;
+  int cnt = 1;
+  cl = x;
+  mask = live ? (1ull << i) : 0ull;
+  while (__ballot(jmp >= 0)) {
+    const int src = jmp >= 0 ? jmp : i;
+    const uint64_t m2 = shfl64(mask, src);
+    const float c2 = __shfl(cl, src, 64);
+    const int n2 = __shfl(cnt, src, 64);
+    const int j2 = __shfl(jmp, src, 64);
+    if (jmp >= 0) {
+      mask |= m2;
+      cl += c2;
+      cnt += n2;
+      jmp = j2;
+    }
+  }
+  depth = cnt - 1;
+  return true;
 }
 
 }  // namespace tl

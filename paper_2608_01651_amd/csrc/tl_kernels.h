@@ -23,6 +23,9 @@ struct VerifyArgs {
   int batch, Hk, Hv, max_nodes, num_slots;
   int tm;          // max_nodes rounded up to a multiple of 16
   float q_scale;
+#ifdef TL_TRACE
+  long long* trace;  // [blocks][16] wall-clock stamps (trace builds only)
+#endif
 };
 
 struct CommitArgs {
