@@ -120,6 +120,9 @@ tl_status tree_state_commit(const tl_problem* problem, const int32_t* node_offse
   a.Hv = problem->num_v_heads;
   a.max_nodes = problem->max_nodes;
   a.num_slots = problem->num_slots;
+#ifdef TL_TRACE
+  a.trace = g_trace;
+#endif
   return tl::launch_commit(*problem, a, reinterpret_cast<hipStream_t>(stream));
 }
 

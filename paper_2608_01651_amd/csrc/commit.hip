@@ -6,10 +6,12 @@
 //   gated linear attention:  S <- gamma S + v k^T
 //   gated delta rule:        u = beta (v - gamma S k),  S <- gamma S + u k^T
 // (stored orientation: S is the slot's [d_v, d_k] matrix).  Rows of the
-// stored state evolve independently under both rules, so one workgroup owns a
-// whole (request, v-head) slot with no cross-workgroup reduction.  Each
-// workgroup reads its whole slot before it writes any of it.  An empty path
-// leaves the slot untouched.
+// stored state evolve independently under both rules (the delta rule's
+// S k is a per-row dot product), so each block of rows is replayed on its
+// own, and nothing crosses workgroups.  A workgroup checks the forest and the
+// path before it writes anything, and every block is read before it is
+// written; an empty path leaves the slot untouched.  The state is read and
+// written once, with non-temporal loads and stores.
 #include <hip/hip_runtime.h>
 
 #include "tl_device.h"
@@ -19,19 +21,33 @@ namespace tl {
 
 constexpr int kCommitChunk = 32;   // path steps staged in LDS at a time
 
+template <int D>
+struct CommitShape {
+  static constexpr int ROWS = (D >= 64) ? 32 : D;   // state rows per streamed block
+  static constexpr int NRB = D / ROWS;              // blocks per (request, v-head) slot
+  static constexpr int LPR = D / 4;                 // lanes per row (4 floats each)
+  static constexpr int RPP = kThreads / LPR;        // rows per pass of the workgroup
+  static constexpr int PASSES = (ROWS + RPP - 1) / RPP;
+};
+
+// One workgroup per (request, v-head) slot.  The path is validated and its
+// rows (k, v, gates) are staged in LDS once; the slot is then streamed in
+// blocks of ROWS rows: while one block is replayed and stored, the next one
+// is already loading.
 template <int MODE, int D, bool F32IN>
 __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
-  constexpr int LPR = D / 4;                        // lanes per state row (4 floats each)
-  constexpr int RPP = kThreads / LPR;               // rows per pass of the block
-  constexpr int PASSES = (D + RPP - 1) / RPP;
+  using SH = CommitShape<D>;
+  constexpr int ROWS = SH::ROWS, NRB = SH::NRB, LPR = SH::LPR, RPP = SH::RPP, PASSES = SH::PASSES;
   constexpr bool GDN = (MODE == TL_MODE_GDN);
   __shared__ __align__(16) float s_k[kCommitChunk * D];
   __shared__ __align__(16) float s_v[kCommitChunk * D];
   __shared__ float s_gam[kCommitChunk];
   __shared__ float s_beta[kCommitChunk];
   __shared__ int s_row[kCommitChunk];
+  __shared__ int s_par[kMaxNodes];
 
   const int tid = threadIdx.x;
+  TL_TRACE_POINT(a, 0);
   const int b = blockIdx.x / a.Hv, h = blockIdx.x % a.Hv;
   const int hq = h / (a.Hv / a.Hk);
 
@@ -49,37 +65,55 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
     if (tid == 0) report(a.dev_err, TL_EINVAL);
     return;
   }
-  // the slot is read first (whole tile into registers) so that its latency
-  // overlaps the checks below; nothing is written before they pass
+  TL_TRACE_POINT(a, 1);
+
+  // the first two blocks are read first so that their latency overlaps the
+  // checks below; nothing is written before they pass
   float* Sp = a.state + ((size_t)sidx * a.Hv + h) * D * D;
   const int col = (tid % LPR) * 4;
-  f32x4 st[PASSES];
-  if (Lp > 0) {
+  const int rsub = tid / LPR;
+  auto load_block = [&](int rb, f32x4 (&st)[PASSES]) {
 #pragma unroll
     for (int p = 0; p < PASSES; ++p) {
-      const int row = p * RPP + tid / LPR;
-      if (row < D) st[p] = *reinterpret_cast<const f32x4*>(Sp + (size_t)row * D + col);
+      const int row = p * RPP + rsub;
+      if (row < ROWS)
+        st[p] = __builtin_nontemporal_load(
+            reinterpret_cast<const f32x4*>(Sp + (size_t)(rb * ROWS + row) * D + col));
     }
+  };
+  auto store_block = [&](int rb, const f32x4 (&st)[PASSES]) {
+#pragma unroll
+    for (int p = 0; p < PASSES; ++p) {
+      const int row = p * RPP + rsub;
+      if (row < ROWS)
+        __builtin_nontemporal_store(st[p], reinterpret_cast<f32x4*>(Sp + (size_t)(rb * ROWS + row) * D + col));
+    }
+  };
+  f32x4 sb[2][PASSES];
+  if (Lp > 0) {
+    load_block(0, sb[0]);
+    if (NRB > 1) load_block(1, sb[1]);
   }
-  // forest of request b (one node per thread)
-  {
-    bool bad = false;
-    if (tid < T) {
-      const int p = a.parent[off + tid];
-      bad = !(p == -1 || (p >= 0 && p < tid));
-    }
-    if (__syncthreads_or(bad)) {
-      if (tid == 0) report(a.dev_err, TL_EBADTREE);
-      return;
-    }
+
+  // forest of request b (one node per thread) and the path, loaded together;
+  // the path's links are then checked against the parents in LDS
+  int par = -1, node = -1;
+  if (tid < T) par = a.parent[off + tid];
+  const bool path_ok = !(Lp > T || (Lp > 0 && a.path == nullptr));
+  if (path_ok && tid < Lp) node = a.path[p0 + tid];
+  if (tid < T) s_par[tid] = par;
+  const bool bad_tree = (tid < T) && !(par == -1 || (par >= 0 && par < tid));
+  const bool node_in = node >= 0 && node < T;
+  TL_TRACE_POINT(a, 2);
+  if (__syncthreads_or(bad_tree)) {
+    if (tid == 0) report(a.dev_err, TL_EBADTREE);
+    return;
   }
-  // path: a root-first chain of request-local nodes
   {
-    bool bad = Lp > T || (Lp > 0 && a.path == nullptr);
+    bool bad = !path_ok;
     if (!bad && tid < Lp) {
-      const int node = a.path[p0 + tid];
       const int want = (tid == 0) ? -1 : a.path[p0 + tid - 1];
-      bad = !(node >= 0 && node < T) || a.parent[off + node] != want;
+      bad = !node_in || s_par[node] != want;
     }
     if (__syncthreads_or(bad)) {
       if (tid == 0) report(a.dev_err, TL_EBADPATH);
@@ -87,11 +121,11 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
     }
   }
   if (Lp == 0) return;
+  TL_TRACE_POINT(a, 3);
 
   const size_t qk_row = (size_t)a.Hk * D, v_row = (size_t)a.Hv * D;
-  for (int c0 = 0; c0 < Lp; c0 += kCommitChunk) {
-    const int n = min(kCommitChunk, Lp - c0);
-    __syncthreads();   // previous chunk fully consumed
+  // stage path steps [c0, c0 + n): row ids and gates, then k and v rows
+  auto stage = [&](int c0, int n) {
     if (tid < n) {
       const int r = off + a.path[p0 + c0 + tid];
       s_row[tid] = r;
@@ -101,18 +135,21 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
     __syncthreads();
     for (int x = tid * 4; x < n * D; x += kThreads * 4) {
       const int t = x / D, e = x % D;
-      const int r = s_row[t];
-      *reinterpret_cast<f32x4*>(s_k + x) = load4<F32IN>(a.k, (size_t)r * qk_row + (size_t)hq * D + e);
-      *reinterpret_cast<f32x4*>(s_v + x) = load4<F32IN>(a.v, (size_t)r * v_row + (size_t)h * D + e);
+      const size_t r = (size_t)s_row[t];
+      *reinterpret_cast<f32x4*>(s_k + x) = load4<F32IN>(a.k, r * qk_row + (size_t)hq * D + e);
+      *reinterpret_cast<f32x4*>(s_v + x) = load4<F32IN>(a.v, r * v_row + (size_t)h * D + e);
     }
     __syncthreads();
+  };
+  // replay staged steps [0, n) on the rows of block rb
+  auto replay = [&](int rb, int n, f32x4 (&st)[PASSES]) {
     for (int t = 0; t < n; ++t) {
       const float gam = s_gam[t];
       const f32x4 kv = *reinterpret_cast<const f32x4*>(s_k + t * D + col);
 #pragma unroll
       for (int p = 0; p < PASSES; ++p) {
-        const int row = p * RPP + tid / LPR;
-        const float vv = s_v[t * D + (row < D ? row : 0)];
+        const int row = p * RPP + rsub;
+        const float vv = s_v[t * D + rb * ROWS + (row < ROWS ? row : 0)];
         if constexpr (!GDN) {
           st[p] = gam * st[p] + vv * kv;
         } else {
@@ -124,12 +161,32 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
         }
       }
     }
-  }
+  };
+
+  if (Lp <= kCommitChunk) {
+    stage(0, Lp);
+    TL_TRACE_POINT(a, 4);
 #pragma unroll
-  for (int p = 0; p < PASSES; ++p) {
-    const int row = p * RPP + tid / LPR;
-    if (row < D) *reinterpret_cast<f32x4*>(Sp + (size_t)row * D + col) = st[p];
+    for (int rb = 0; rb < NRB; ++rb) {
+      replay(rb, Lp, sb[rb & 1]);
+      store_block(rb, sb[rb & 1]);
+      if (rb + 2 < NRB) load_block(rb + 2, sb[rb & 1]);
+    }
+  } else {
+    // long paths: the steps are staged chunk by chunk for every block
+#pragma unroll
+    for (int rb = 0; rb < NRB; ++rb) {
+      for (int c0 = 0; c0 < Lp; c0 += kCommitChunk) {
+        const int n = min(kCommitChunk, Lp - c0);
+        __syncthreads();   // the previous chunk is fully consumed
+        stage(c0, n);
+        replay(rb, n, sb[rb & 1]);
+      }
+      store_block(rb, sb[rb & 1]);
+      if (rb + 2 < NRB) load_block(rb + 2, sb[rb & 1]);
+    }
   }
+  TL_TRACE_POINT(a, 5);
 }
 
 template <int MODE, int D, bool F32IN>

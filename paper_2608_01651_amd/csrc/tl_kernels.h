@@ -41,6 +41,9 @@ struct CommitArgs {
   const int32_t* slot;
   int32_t* dev_err;
   int batch, Hk, Hv, max_nodes, num_slots;
+#ifdef TL_TRACE
+  long long* trace;  // [blocks][16] wall-clock stamps (trace builds only)
+#endif
 };
 
 struct TopoArgs {

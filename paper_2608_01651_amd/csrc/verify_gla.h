@@ -118,8 +118,8 @@ __device__ inline void verify_gla_mfma(const VerifyArgs& a, const Unit u) {
         const float* row = Sp + (size_t)(kTile * mt + lr) * D;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          sr[m][ks][0] = *reinterpret_cast<const f32x4*>(row + ks * 32 + 4 * lg);
-          sr[m][ks][1] = *reinterpret_cast<const f32x4*>(row + ks * 32 + 16 + 4 * lg);
+          sr[m][ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 4 * lg));
+          sr[m][ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 16 + 4 * lg));
         }
       }
     }
@@ -349,7 +349,8 @@ __device__ inline void verify_gla_mfma(const VerifyArgs& a, const Unit u) {
 #pragma unroll
         for (int m = 0; m < MT; ++m) {
           const int mt = wave + kWaves * m;
-          if (mt < MTILES) *reinterpret_cast<f32x4*>(orow + kTile * mt + 4 * lg) = a.q_scale * acc[m];
+          if (mt < MTILES)
+            __builtin_nontemporal_store(a.q_scale * acc[m], reinterpret_cast<f32x4*>(orow + kTile * mt + 4 * lg));
         }
       }
     }
