@@ -31,11 +31,11 @@ struct CommitShape {
 };
 
 // One workgroup per (request, v-head) slot.  The path is validated and its
-// rows (k, v, gates) are staged in LDS once; the slot is then streamed in
-// blocks of ROWS rows: while one block is replayed and stored, the next one
-// is already loading.
+// rows (k, v, gates) are staged in LDS once; the slot is then replayed and
+// stored in blocks of ROWS rows, whose loads are all issued at the start
+// (delta rule: two blocks at a time).
 template <int MODE, int D, bool F32IN>
-__global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void commit_kernel(CommitArgs a) {
   using SH = CommitShape<D>;
   constexpr int ROWS = SH::ROWS, NRB = SH::NRB, LPR = SH::LPR, RPP = SH::RPP, PASSES = SH::PASSES;
   constexpr bool GDN = (MODE == TL_MODE_GDN);
@@ -67,8 +67,8 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
   }
   TL_TRACE_POINT(a, 1);
 
-  // the first two blocks are read first so that their latency overlaps the
-  // checks below; nothing is written before they pass
+  // state blocks are read first so that their latency overlaps the checks
+  // below; nothing is written before they pass
   float* Sp = a.state + ((size_t)sidx * a.Hv + h) * D * D;
   const int col = (tid % LPR) * 4;
   const int rsub = tid / LPR;
@@ -89,10 +89,14 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
         __builtin_nontemporal_store(st[p], reinterpret_cast<f32x4*>(Sp + (size_t)(rb * ROWS + row) * D + col));
     }
   };
-  f32x4 sb[2][PASSES];
+  // gated linear attention keeps every block of the slot in registers (all
+  // loads in flight at once); the delta rule needs more registers for its
+  // row reductions and streams the blocks through two buffers
+  constexpr int NBUF = GDN ? (NRB < 2 ? NRB : 2) : NRB;
+  f32x4 sb[NBUF][PASSES];
   if (Lp > 0) {
-    load_block(0, sb[0]);
-    if (NRB > 1) load_block(1, sb[1]);
+#pragma unroll
+    for (int rb = 0; rb < NBUF; ++rb) load_block(rb, sb[rb]);
   }
 
   // forest of request b (one node per thread) and the path, loaded together;
@@ -168,9 +172,9 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
     TL_TRACE_POINT(a, 4);
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb) {
-      replay(rb, Lp, sb[rb & 1]);
-      store_block(rb, sb[rb & 1]);
-      if (rb + 2 < NRB) load_block(rb + 2, sb[rb & 1]);
+      replay(rb, Lp, sb[rb % NBUF]);
+      store_block(rb, sb[rb % NBUF]);
+      if (rb + NBUF < NRB) load_block(rb + NBUF, sb[rb % NBUF]);
     }
   } else {
     // long paths: the steps are staged chunk by chunk for every block
@@ -180,10 +184,10 @@ __global__ __launch_bounds__(kThreads) void commit_kernel(CommitArgs a) {
         const int n = min(kCommitChunk, Lp - c0);
         __syncthreads();   // the previous chunk is fully consumed
         stage(c0, n);
-        replay(rb, n, sb[rb & 1]);
+        replay(rb, n, sb[rb % NBUF]);
       }
-      store_block(rb, sb[rb & 1]);
-      if (rb + 2 < NRB) load_block(rb + 2, sb[rb & 1]);
+      store_block(rb, sb[rb % NBUF]);
+      if (rb + NBUF < NRB) load_block(rb + NBUF, sb[rb % NBUF]);
     }
   }
   TL_TRACE_POINT(a, 5);

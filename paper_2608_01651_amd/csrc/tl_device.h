@@ -51,6 +51,34 @@ __device__ inline void split_bf16(float x, __bf16& hi, __bf16& lo) {
   lo = (__bf16)(x - (float)hi);
 }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Two fp32 values -> bf16 hi pair + bf16 lo pair (one 32-bit word each,
+// element 0 in the low half).  hi is x with its low 16 bits cleared
+// (truncation), so x - hi is exact in fp32 and |x - hi| < 2^-7 |x|; lo is that
+// remainder rounded to nearest, so hi + lo == x to 2^-16 relative.  Costs one
+// byte permute for the two hi values, and an AND, a subtract and half a
+// convert per value for lo.
+__device__ inline void split2_bf16(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+  const uint32_t b0 = __float_as_uint(x0), b1 = __float_as_uint(x1);
+  hi = __builtin_amdgcn_perm(b1, b0, 0x07060302u);   // high halves of b0 (low) and b1 (high)
+  const float l0 = x0 - __uint_as_float(b0 & 0xffff0000u);
+  const float l1 = x1 - __uint_as_float(b1 & 0xffff0000u);
+  lo = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)l0, (__bf16)l1});
+}
+
+// Eight fp32 values (a then b) -> bf16x8 hi and lo operands (split2_bf16).
+__device__ inline void split8_bf16(const f32x4& a, const f32x4& b, bf16x8& hi, bf16x8& lo) {
+  uint32_t h0, h1, h2, h3, l0, l1, l2, l3;
+  split2_bf16(a[0], a[1], h0, l0);
+  split2_bf16(a[2], a[3], h1, l1);
+  split2_bf16(b[0], b[1], h2, l2);
+  split2_bf16(b[2], b[3], h3, l3);
+  hi = __builtin_bit_cast(bf16x8, u32x4{h0, h1, h2, h3});
+  lo = __builtin_bit_cast(bf16x8, u32x4{l0, l1, l2, l3});
+}
+
 // 4 consecutive inputs as floats, from bf16 or fp32 storage.
 template <bool F32IN>
 __device__ inline f32x4 load4(const void* base, size_t idx) {
@@ -203,9 +231,51 @@ __device__ inline void copy16_to_lds(const void* gsrc, void* lds_base) {
   __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
 }
 
+// The same copy, issued as inline assembly: the compiler does not see the
+// LDS write, so it does not hold later LDS accesses behind every outstanding
+// load of the wave (it would have to assume they alias the copy).  The
+// caller must wait for completion itself (wait_vmem / wait_vmem_below)
+// before the copied bytes are read.  M0 (the LDS base of the copy) is saved
+// and restored around it, so no register the compiler owns is changed; one
+// wait state separates each M0 write from the next instruction that reads it.
+__device__ inline void copy16_to_lds_async(const void* gsrc, void* lds_base) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds_base);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0"
+      : "=&s"(saved)
+      : "v"(gsrc), "s"(m0v)
+      : "memory");
+}
+
 // Waits for every outstanding vector memory operation of this wave
 // (including the direct-to-LDS copies).
 __device__ inline void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Waits until at most N vector memory operations of this wave are
+// outstanding.  Loads complete in issue order, so everything issued before
+// the last N has landed (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
+// and lgkmcnt left at their maxima).
+template <int N>
+__device__ inline void wait_vmem_below() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier for LDS data: this wave's LDS accesses complete, then
+// s_barrier.  Unlike __syncthreads() it does not wait for the wave's
+// outstanding global loads, so loads issued for later phases stay in flight.
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Compiler-only fence: keeps the compiler from moving memory operations
+// across this point (issue order matters for wait_vmem_below).
+__device__ inline void issue_fence() { asm volatile("" ::: "memory"); }
 
 // Rows of CPR 16-byte chunks are stored with chunk c at position
 // c ^ (row & (CPR-1)) so that the same column of 16 consecutive rows falls in

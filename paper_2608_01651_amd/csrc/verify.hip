@@ -34,7 +34,8 @@
 // Vector path (fp32 inputs, d = 16, trees of fewer than 16 nodes): the same
 // steps with vector ALU products.
 //
-// Files: verify_gla.h (gated linear attention on MFMA), verify_gdn.h (delta
+// Files: verify_gla_small.h (gated linear attention on MFMA, trees of <= 64
+// nodes), verify_gla.h (the same for larger trees), verify_gdn.h (delta
 // rule on MFMA), verify_vector.h (vector path), verify_common.h (layouts).
 #include <hip/hip_runtime.h>
 
@@ -43,22 +44,24 @@
 #include "verify_common.h"
 #include "verify_gdn.h"
 #include "verify_gla.h"
+#include "verify_gla_small.h"
 #include "verify_vector.h"
 
 namespace tl {
 
-template <int MODE, int D, int BV, bool F32IN, int W>
-__global__ __launch_bounds__(kThreads) void verify_kernel(VerifyArgs a) {
+template <int MODE, int D, int BV, bool F32IN, int W, int NH>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NH == 2 ? 2 : 1))) void verify_kernel(VerifyArgs a) {
   constexpr int NSL = D / BV;              // value slices per head
   constexpr bool CAN_MFMA = !F32IN && D >= 32;
   const int tid = threadIdx.x;
   TL_TRACE_POINT(a, 0);
 
-  // ---- block -> (request, qk-head, v-head, slice).  Consecutive block ids go
-  // to different XCDs (round robin over 8); all blocks that read the same
-  // request's q/k rows are given ids 8 apart so they share one XCD's L2.
+  // ---- block -> (request, qk-head, first v-head, slice).  A block serves NH
+  // v-heads of one qk-head.  Consecutive block ids go to different XCDs
+  // (round robin over 8); all blocks that read the same request's q/k rows
+  // are given ids 8 apart so they share one XCD's L2.
   const int grp = a.Hv / a.Hk;
-  const int GS = grp * NSL;
+  const int GS = (grp / NH) * NSL;
   const int nshare = a.batch * a.Hk;
   const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
   const int sh = (local / GS) * 8 + xcd;
@@ -67,7 +70,7 @@ __global__ __launch_bounds__(kThreads) void verify_kernel(VerifyArgs a) {
   Unit u;
   u.b = sh / a.Hk;
   u.hq = sh % a.Hk;
-  u.h = u.hq * grp + w_in / NSL;
+  u.h = u.hq * grp + (w_in / NSL) * NH;
   u.slice = w_in % NSL;
   u.tm = a.tm;
 
@@ -83,35 +86,46 @@ __global__ __launch_bounds__(kThreads) void verify_kernel(VerifyArgs a) {
   }
   if constexpr (CAN_MFMA) {
     if (u.T >= kTile) {
-      if constexpr (MODE == TL_MODE_GLA) verify_gla_mfma<D, BV, W>(a, u);
-      else verify_gdn_mfma<MODE, D, BV, W>(a, u);
+      if constexpr (MODE == TL_MODE_GLA) {
+        if constexpr (W == 1) verify_gla_small<D, BV, NH>(a, u);
+        else verify_gla_mfma<D, BV, W>(a, u);
+      } else {
+        verify_gdn_mfma<MODE, D, BV, W>(a, u);
+      }
       TL_TRACE_POINT(a, 15);
       return;
     }
   }
-  verify_vector<MODE, D, BV, F32IN, W>(a, u);
+#pragma unroll
+  for (int hh = 0; hh < NH; ++hh) {
+    if (hh) __syncthreads();   // the previous head is done with the LDS
+    Unit uh = u;
+    uh.h = u.h + hh;
+    verify_vector<MODE, D, BV, F32IN, W>(a, uh);
+  }
 }
 
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
-template <int MODE, int D, int BV, bool F32IN, int W>
+template <int MODE, int D, int BV, bool F32IN, int W, int NH>
 static tl_status launch_one(const VerifyArgs& a, hipStream_t stream) {
   constexpr int NSL = D / BV;
   constexpr bool CAN_MFMA = !F32IN && D >= 32;
   // a block may take the vector path or (at least 16 nodes) the MFMA path
   VerifyLayout L = verify_layout(MODE, D, BV, F32IN ? 4 : 2, a.tm, W, false);
   if (CAN_MFMA) {
-    const int t = (MODE == TL_MODE_GLA) ? gla_layout(D, BV, a.tm, W).total
-                                        : verify_layout(MODE, D, BV, 2, a.tm, W, true).total;
+    int t;
+    if (MODE == TL_MODE_GLA) t = (W == 1) ? gla_small_layout(D, BV, NH).total : gla_layout(D, BV, a.tm, W).total;
+    else t = verify_layout(MODE, D, BV, 2, a.tm, W, true).total;
     if (t > L.total) L.total = t;
   }
   const int grp = a.Hv / a.Hk;
   const long nshare = (long)a.batch * a.Hk;
-  const long blocks = 8 * ((nshare + 7) / 8) * grp * NSL;
+  const long blocks = 8 * ((nshare + 7) / 8) * (grp / NH) * NSL;
   if (blocks == 0) return TL_OK;
   if (blocks > 0x7fffffffL) return TL_EINVAL;
-  auto kern = verify_kernel<MODE, D, BV, F32IN, W>;
+  auto kern = verify_kernel<MODE, D, BV, F32IN, W, NH>;
   if (L.total > 160 * 1024) return TL_EUNSUPPORTED;
   if (L.total > 64 * 1024) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -124,16 +138,21 @@ static tl_status launch_one(const VerifyArgs& a, hipStream_t stream) {
 
 // W = 64-bit words per ancestor mask (trees of <= 64, 128, 256 nodes).  The
 // delta rule with d = 128 keeps U [tm][BV] in LDS, so 256-node trees use
-// 32-column value slices to stay within the 160 KB of LDS.
+// 32-column value slices to stay within the 160 KB of LDS.  Gated linear
+// attention over trees of <= 64 nodes serves two grouped v-heads per block
+// when the group size is even.
 template <int MODE, int D, int BV, bool F32IN>
 static tl_status dispatch_w(const VerifyArgs& a, hipStream_t stream) {
-  if (F32IN) return launch_one<MODE, D, BV, F32IN, 4>(a, stream);
+  if (F32IN) return launch_one<MODE, D, BV, F32IN, 4, 1>(a, stream);
   if (a.tm > 128) {
-    if constexpr (MODE == TL_MODE_GDN && D == 128) return launch_one<MODE, D, 32, F32IN, 4>(a, stream);
-    return launch_one<MODE, D, BV, F32IN, 4>(a, stream);
+    if constexpr (MODE == TL_MODE_GDN && D == 128) return launch_one<MODE, D, 32, F32IN, 4, 1>(a, stream);
+    return launch_one<MODE, D, BV, F32IN, 4, 1>(a, stream);
   }
-  if (a.tm > 64) return launch_one<MODE, D, BV, F32IN, 2>(a, stream);
-  return launch_one<MODE, D, BV, F32IN, 1>(a, stream);
+  if (a.tm > 64) return launch_one<MODE, D, BV, F32IN, 2, 1>(a, stream);
+  if constexpr (MODE == TL_MODE_GLA && D >= 32) {
+    if ((a.Hv / a.Hk) % 2 == 0) return launch_one<MODE, D, BV, F32IN, 1, 2>(a, stream);
+  }
+  return launch_one<MODE, D, BV, F32IN, 1, 1>(a, stream);
 }
 
 template <int MODE, bool F32IN>

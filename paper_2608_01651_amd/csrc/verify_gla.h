@@ -25,9 +25,17 @@ struct GlaLayout {
   int x, cl, mask, tmask, qst, kst, vt, total;
 };
 
-// LDS layout of the MFMA path (bytes).  V^T rows have stride tm + 8
-// elements: (tm + 8) / 2 = 4 (mod 8) 32-bit words, so the 8-byte fragment
-// reads of 16 rows by 4 lane groups hit 64 different banks.
+// V^T row stride (elements): the tree term reads whole 32-node chunks, so
+// rows hold 32 * ceil(tm / 32) columns, plus 8: stride / 2 = 4 (mod 8) 32-bit
+// words, so the 8-byte fragment reads of 16 rows by 4 lane groups hit 64
+// different banks.
+__host__ __device__ constexpr int gla_vt_stride(int tm) { return ((tm + 31) & ~31) + 8; }
+
+// C operand fragments of a tree of nt node tiles (trees of <= 64 nodes): tile
+// I uses I / 2 + 1 chunks of 32 ancestor columns.
+__host__ __device__ constexpr int gla_small_slots(int nt) { return (nt * nt + 2 * nt + (nt & 1)) / 4; }
+
+// LDS layout of the MFMA paths (bytes).
 __host__ __device__ inline GlaLayout gla_layout(int D, int BV, int tm, int W) {
   GlaLayout L;
   int o = 0;
@@ -37,8 +45,8 @@ __host__ __device__ inline GlaLayout gla_layout(int D, int BV, int tm, int W) {
   L.tmask = o; o += align16((tm / kTile) * W * 8);       // OR of M+ rows per node tile
   L.qst = o;   o += (W == 1) ? tm * D * 2 : 0;           // Q rows (trees of <= 64 nodes)
   L.kst = o;   o += tm * D * 2;                          // K rows, swizzled bf16
-  L.vt = o;                                              // V^T [BV][tm + 8] bf16
-  const int vt = BV * (tm + 8) * 2;
+  L.vt = o;                                              // V^T [BV][stride] bf16
+  const int vt = BV * gla_vt_stride(tm) * 2;
   const int topo = kThreads * (4 + 4 + 4) + kThreads * W * 8;   // aliases V^T (prologue only)
   o += align16(vt > topo ? vt : topo);
   L.total = o;
@@ -58,7 +66,7 @@ __device__ inline void verify_gla_mfma(const VerifyArgs& a, const Unit u) {
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, lr = lane & 15, lg = lane >> 4;
   const int T = u.T, off = u.off, hq = u.hq, tm = u.tm, slice = u.slice;
-  const int TS = tm + 8;
+  const int TS = gla_vt_stride(tm);
   const GlaLayout L = gla_layout(D, BV, tm, W);
   float* s_x = reinterpret_cast<float*>(tl_lds + L.x);
   float* s_cl = reinterpret_cast<float*>(tl_lds + L.cl);
