@@ -217,11 +217,11 @@ def _cpu_prefix(args):
 
 
 def _cpu_request(args):
-    cfg_name, seed, b, state = args
+    cfg_name, seed, step, b, state = args
     import oracle
     from synth import workloads as W
     cfg = W.CONFIGS[cfg_name]
-    w = W.make(cfg, seed=seed, requests=[b])
+    w = W.make(cfg, seed=seed, step=step, requests=[b])
     oracle.verify(cfg.mode, cfg.num_qk_heads, w.node_offsets, w.parent, w.q, w.k, w.v, w.g,
                   w.beta, state, q_scale=cfg.q_scale, max_nodes=cfg.max_nodes)
     oracle.commit(cfg.mode, cfg.num_qk_heads, w.node_offsets, w.parent, w.path_offsets, w.path,
@@ -230,22 +230,28 @@ def _cpu_request(args):
 
 
 def cpu_baseline(args, cfg, log):
+    """The fp64 oracle on a bounded sample: whole steps of up to 32 requests
+    of the same workload (each step draws new trees; a request's S_pre is its
+    prefix state), repeated until about args.cpu_seconds of wall time."""
     import concurrent.futures as cf
     import multiprocessing as mp
-    from synth import workloads as W
     cores = len(os.sched_getaffinity(0))
-    cores = max(1, min(cores, 16, cfg.batch))
-    nreq = min(cfg.batch, max(cores, args.cpu_requests))
-    reqs = list(range(nreq))
+    cores = max(1, min(cores, 16))
+    reqs = list(range(min(cfg.batch, 32)))
     ctx = mp.get_context("fork")
     with cf.ProcessPoolExecutor(max_workers=cores, mp_context=ctx, initializer=_cpu_init) as ex:
         states = list(ex.map(_cpu_prefix, [(cfg.name, args.seed, b) for b in reqs]))
         # the timed region covers drawing each request's tree inputs (cheap)
         # and the oracle's verify + commit of it
         t0 = time.perf_counter()
-        nodes = sum(ex.map(_cpu_request, [(cfg.name, args.seed, b, s) for b, s in zip(reqs, states)]))
-        dt = time.perf_counter() - t0
-    log(f"oracle: {nodes} nodes of {nreq} requests in {dt:.2f} s on {cores} processes")
+        nodes = steps = 0
+        while True:
+            nodes += sum(ex.map(_cpu_request, [(cfg.name, args.seed, steps, b, states[b]) for b in reqs]))
+            steps += 1
+            dt = time.perf_counter() - t0
+            if dt >= args.cpu_seconds or steps >= 256:
+                break
+    log(f"oracle: {nodes} nodes in {steps} steps of {len(reqs)} requests, {dt:.2f} s on {cores} processes")
     cpu_model = ""
     try:
         for line in open("/proc/cpuinfo"):
@@ -255,8 +261,8 @@ def cpu_baseline(args, cfg, log):
     except OSError:
         pass
     return {"value": nodes / dt, "unit": "tree-tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"fp64 oracle verify+commit of requests 0..{nreq - 1} of the {cfg.name} "
-                      f"workload ({nodes} tree nodes), one process per core, "
+            "sample": f"fp64 oracle verify+commit of {steps} steps x requests 0..{len(reqs) - 1} of the "
+                      f"{cfg.name} workload ({nodes} tree nodes), one process per core, "
                       f"{dt:.2f} s wall; CPU: {cpu_model}"}
 
 
@@ -307,7 +313,8 @@ def main():
                     choices=["tiny", "mid", "production", "gdn", "large"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--layers", type=int, default=0, help="layer buffer sets (0: auto)")
-    ap.add_argument("--cpu-requests", type=int, default=16)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="wall time of the oracle sample (whole steps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",

@@ -1,0 +1,142 @@
+"""The C-ABI library without a GPU: it loads, exports every function that
+include/treelin.h declares, and its synchronous argument checks return the
+documented codes before any device call (every case below fails a host
+check, so nothing is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_01651_amd import treelin as tl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _lib_or_build():
+    if not os.path.exists(tl._LIB_PATH):
+        from paper_2608_01651_amd import build
+        build.build()
+    return tl.lib()
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "treelin.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\*?\s*([A-Za-z_][A-Za-z0-9_]*)\s*\(",
+                       text, flags=re.M)
+    return sorted(set(n for n in names if n not in ("if", "while", "return", "sizeof")))
+
+
+def test_library_exports_every_declared_function():
+    L = _lib_or_build()
+    names = _declared_functions()
+    assert {"tree_lin_attn_verify", "tree_state_commit", "tree_topology_export",
+            "tl_status_string", "tl_version"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in include/treelin.h but not exported"
+
+
+def test_status_strings_and_version():
+    _lib_or_build()
+    for code in range(6):
+        assert tl.status_string(code).startswith(
+            ("TL_OK", "TL_EINVAL", "TL_EBADTREE", "TL_EBADPATH", "TL_EUNSUPPORTED", "TL_EHIP"))
+    assert "unknown" in tl.status_string(99)
+    assert re.fullmatch(r"\d+\.\d+\.\d+", tl.version())
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    monkeypatch.setattr(tl, "_LIB_PATH", os.path.join(ROOT, "no_such_lib.so"))
+    monkeypatch.setattr(tl, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        tl.lib()
+
+
+# fake, never dereferenced device addresses (every case fails a host check first)
+A16 = 0x10000
+MIS = 0x10002
+
+
+def _verify(prob, q=A16, k=A16, v=A16, g=A16, beta=None, state=A16, out=A16, offs=A16, par=A16,
+            slot=None, err=None):
+    return _lib_or_build().tree_lin_attn_verify(
+        None if prob is None else ctypes.byref(prob), offs, par, q, k, v, g, beta, state, slot, out,
+        err, None)
+
+
+def _commit(prob, path_offsets=A16, path=A16, k=A16, v=A16, g=A16, beta=None, state=A16):
+    return _lib_or_build().tree_state_commit(
+        None if prob is None else ctypes.byref(prob), A16, A16, path_offsets, path, k, v, g, beta,
+        state, None, None, None)
+
+
+def _topology(prob, mask=A16, depth=A16):
+    return _lib_or_build().tree_topology_export(
+        None if prob is None else ctypes.byref(prob), A16, A16, mask, depth, None, None)
+
+
+def P(**kw):
+    base = dict(batch=2, num_qk_heads=2, num_v_heads=4, d_k=64, d_v=64, max_nodes=64)
+    base.update({k: v for k, v in kw.items() if k in base})
+    extra = {k: v for k, v in kw.items() if k not in base}
+    return tl.problem(**base, **extra)
+
+
+@pytest.mark.parametrize("prob, code", [
+    (None, tl.TL_EINVAL),
+    (P(num_v_heads=3), tl.TL_EINVAL),            # Hv % Hk != 0
+    (P(num_qk_heads=0), tl.TL_EINVAL),
+    (P(batch=-1), tl.TL_EINVAL),
+    (P(mode=7), tl.TL_EINVAL),
+    (P(in_dtype=3), tl.TL_EINVAL),
+    (P(d_k=48, d_v=48), tl.TL_EUNSUPPORTED),
+    (P(d_k=256, d_v=256), tl.TL_EUNSUPPORTED),
+    (P(d_v=32), tl.TL_EUNSUPPORTED),             # d_v != d_k
+    (P(max_nodes=0), tl.TL_EUNSUPPORTED),
+    (P(max_nodes=257), tl.TL_EUNSUPPORTED),
+    (P(num_slots=0), tl.TL_EINVAL),
+])
+def test_problem_checks(prob, code):
+    assert _verify(prob) == code
+    assert _commit(prob) == code
+    assert _topology(prob) == code
+
+
+def test_empty_batch_is_a_no_op():
+    # nothing is launched and no pointer is needed
+    prob = P(batch=0)
+    assert _verify(prob, q=None, k=None, v=None, g=None, state=None, out=None, offs=None, par=None) == tl.TL_OK
+    assert _commit(prob, path_offsets=None, path=None, k=None, v=None, g=None, state=None) == tl.TL_OK
+    assert _topology(prob, mask=None, depth=None) == tl.TL_OK
+
+
+@pytest.mark.parametrize("field", ["q", "k", "v", "g", "state", "out", "offs", "par"])
+def test_verify_null_pointers(field):
+    assert _verify(P(), **{field: None}) == tl.TL_EINVAL
+
+
+@pytest.mark.parametrize("field", ["q", "k", "v", "state", "out"])
+def test_verify_misaligned_pointers(field):
+    assert _verify(P(), **{field: MIS}) == tl.TL_EINVAL
+
+
+def test_beta_presence_must_match_the_rule():
+    assert _verify(P(mode=tl.GLA), beta=A16) == tl.TL_EINVAL
+    assert _verify(P(mode=tl.GDN), beta=None) == tl.TL_EINVAL
+    assert _commit(P(mode=tl.GLA), beta=A16) == tl.TL_EINVAL
+    assert _commit(P(mode=tl.GDN), beta=None) == tl.TL_EINVAL
+
+
+def test_identity_slots_need_enough_slots():
+    assert _verify(P(batch=4, num_slots=3)) == tl.TL_EINVAL
+
+
+def test_commit_and_topology_pointer_checks():
+    assert _commit(P(), path_offsets=None) == tl.TL_EINVAL
+    assert _commit(P(), path_offsets=A16 + 2) == tl.TL_EINVAL
+    assert _commit(P(), path=A16 + 2) == tl.TL_EINVAL
+    assert _topology(P(), mask=None) == tl.TL_EINVAL
+    assert _topology(P(), mask=A16 + 4) == tl.TL_EINVAL
+    assert _topology(P(), depth=None) == tl.TL_EINVAL

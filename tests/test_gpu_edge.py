@@ -1,0 +1,375 @@
+"""GPU edge cases through the C ABI, against the fp64 oracle: device error
+reporting (the bad request is skipped, the others are computed), empty
+paths and requests, slot indirection, determinism, several verify -> commit
+steps with carried state, other head dimensions and group sizes, forests
+with several roots, the deepest tree (a 256-node chain), a query scale, and
+the full production batch in the benchmark's launch configuration."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import workloads as W
+from tests import gpu_helpers as H
+from paper_2608_01651_amd import treelin as tl
+
+pytestmark = pytest.mark.gpu
+
+
+def cfg_of(base, **kw):
+    return dataclasses.replace(W.CONFIGS[base], **kw)
+
+
+def custom(cfg, parents, paths, seed=0):
+    """A workload over explicit forests: q/k unit rows, v ~ N(0,1), gates and
+    beta drawn like the configuration's, stored in its input dtype."""
+    rng = np.random.default_rng([seed, 4242])
+    Hk, Hv, dk, dv = cfg.num_qk_heads, cfg.num_v_heads, cfg.d_k, cfg.d_v
+    sizes = [len(p) for p in parents]
+    N = int(sum(sizes))
+
+    def store(x):
+        x = np.asarray(x, np.float32)
+        return W.round_bf16(x) if cfg.in_dtype == "bf16" else x
+
+    def unit(shape):
+        x = rng.standard_normal(shape)
+        return store(x / np.linalg.norm(x, axis=-1, keepdims=True))
+
+    g = (-np.logaddexp(0.0, rng.standard_normal((N, Hv)) - cfg.gate_shift)).astype(np.float32)
+    beta = None
+    if cfg.mode == W.GDN:
+        beta = (1.0 / (1.0 + np.exp(-rng.standard_normal((N, Hv))))).astype(np.float32)
+    return W.Workload(
+        cfg=cfg, seed=seed, step=0,
+        node_offsets=np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32),
+        parent=np.concatenate([np.asarray(p, np.int32) for p in parents]) if N else np.zeros(0, np.int32),
+        q=unit((N, Hk, dk)), k=unit((N, Hk, dk)), v=store(rng.standard_normal((N, Hv, dv))),
+        g=g, beta=beta,
+        path_offsets=np.concatenate([[0], np.cumsum([len(p) for p in paths])]).astype(np.int32),
+        path=np.concatenate([np.asarray(p, np.int32) for p in paths]) if sum(map(len, paths))
+        else np.zeros(0, np.int32),
+        state=None)
+
+
+def rand_state(cfg, slots, seed=0, scale=0.3):
+    rng = np.random.default_rng([seed, 777])
+    return (scale * rng.standard_normal((slots, cfg.num_v_heads, cfg.d_v, cfg.d_k))).astype(np.float32)
+
+
+def o_verify(cfg, w, state, slot=None, max_nodes=None):
+    return oracle.verify(cfg.mode, cfg.num_qk_heads, w.node_offsets, w.parent, w.q, w.k, w.v, w.g,
+                         w.beta, state, slot=slot, q_scale=cfg.q_scale,
+                         max_nodes=max_nodes or cfg.max_nodes)
+
+
+def o_commit(cfg, w, state, slot=None, max_nodes=None):
+    return oracle.commit(cfg.mode, cfg.num_qk_heads, w.node_offsets, w.parent, w.path_offsets,
+                         w.path, w.k, w.v, w.g, w.beta, state, slot=slot,
+                         max_nodes=max_nodes or cfg.max_nodes)
+
+
+def sub(w, keep):
+    """Requests `keep` of w as a workload of their own (for oracle references)."""
+    reqs = []
+    for b in keep:
+        o0, o1 = int(w.node_offsets[b]), int(w.node_offsets[b + 1])
+        p0, p1 = int(w.path_offsets[b]), int(w.path_offsets[b + 1])
+        reqs.append((o0, o1, p0, p1))
+    cat = lambda x: np.concatenate([x[o0:o1] for o0, o1, _, _ in reqs]) if x is not None else None
+    return dataclasses.replace(
+        w, node_offsets=np.concatenate([[0], np.cumsum([o1 - o0 for o0, o1, _, _ in reqs])]).astype(np.int32),
+        parent=cat(w.parent), q=cat(w.q), k=cat(w.k), v=cat(w.v), g=cat(w.g), beta=cat(w.beta),
+        path_offsets=np.concatenate([[0], np.cumsum([p1 - p0 for _, _, p0, p1 in reqs])]).astype(np.int32),
+        path=np.concatenate([w.path[p0:p1] for _, _, p0, p1 in reqs]).astype(np.int32))
+
+
+def rows_of(w, keep):
+    return np.concatenate([np.arange(w.node_offsets[b], w.node_offsets[b + 1]) for b in keep])
+
+
+def topk(T, seed):
+    return W.topk_tree(np.random.default_rng([seed, 11]), T, (8, 4, 2), 10)
+
+
+def chain_path(parent, node):
+    return W.path_to(parent, node)
+
+
+# ----------------------------------------------------------------------------
+# device-side errors: reported once, the request skipped, the others computed
+# ----------------------------------------------------------------------------
+
+ERROR_CONFIGS = [
+    ("production", dict()),                                    # <= 64 nodes, two heads per block
+    ("mid", dict()),                                           # <= 64 nodes, one head per block
+    ("gdn", dict(max_nodes=128)),                              # delta rule
+    ("large", dict()),                                         # 65..256 nodes
+    ("tiny", dict()),                                          # vector path
+]
+
+
+def _error_case(name, kw, T=40):
+    cfg = cfg_of(name, batch=3, prefix_len=0, **kw)
+    if name == "tiny":
+        T = 15
+    parents = [topk(T, s) if T > 15 else W.binary_tree(3) for s in range(3)]
+    paths = [chain_path(p, int(np.flatnonzero(W.node_depths(p) == W.node_depths(p).max())[0]))
+             for p in parents]
+    return cfg, parents, paths
+
+
+@pytest.mark.parametrize("name, kw", ERROR_CONFIGS)
+def test_bad_parent_is_reported_and_skipped(name, kw):
+    cfg, parents, paths = _error_case(name, kw)
+    bad = [p.copy() for p in parents]
+    bad[1][5] = 9                       # a parent after its child
+    w = custom(cfg, bad, paths)
+    state = rand_state(cfg, 3)
+    up = H.Uploaded(w)
+    got, err = H.run_verify(cfg, up, H.t_f32(state))
+    assert err == tl.TL_EBADTREE
+    good = [0, 2]
+    ref = o_verify(cfg, sub(w, good), state[good])
+    rows = rows_of(w, good)
+    assert H.slice_rel_err(got[rows], ref, sub(w, good).node_offsets) <= H.TOL
+    assert np.isnan(got[rows_of(w, [1])]).all(), "the bad request's rows must stay unwritten"
+    st = H.t_f32(state)
+    err = H.run_commit(cfg, up, st)
+    assert err == tl.TL_EBADTREE
+    after = st.cpu().numpy()
+    np.testing.assert_array_equal(after[1], state[1])
+    ref_s = o_commit(cfg, sub(w, good), state[good])
+    assert H.state_rel_err(after[good], ref_s) <= H.TOL
+
+
+@pytest.mark.parametrize("how", ["not_a_root", "broken_link", "out_of_range", "too_long"])
+def test_bad_path_is_reported_and_slot_untouched(how):
+    cfg, parents, paths = _error_case("production", {})
+    paths = [list(p) for p in paths]
+    if how == "not_a_root":
+        paths[1] = paths[1][1:]
+    elif how == "broken_link":
+        paths[1] = [paths[1][0]] + paths[1][2:]
+    elif how == "out_of_range":
+        paths[1] = paths[1][:-1] + [len(parents[1]) + 3]
+    else:
+        paths[1] = list(range(len(parents[1]))) + [0]
+    w = custom(cfg, parents, paths)
+    state = rand_state(cfg, 3)
+    st = H.t_f32(state)
+    err = H.run_commit(cfg, H.Uploaded(w), st)
+    assert err == tl.TL_EBADPATH
+    after = st.cpu().numpy()
+    np.testing.assert_array_equal(after[1], state[1])
+    good = [0, 2]
+    assert H.state_rel_err(after[good], o_commit(cfg, sub(w, good), state[good])) <= H.TOL
+
+
+def test_tree_larger_than_max_nodes_is_reported():
+    cfg = cfg_of("production", batch=2, prefix_len=0)
+    w = custom(cfg, [topk(64, 1), topk(64, 2)], [[0], [0]])
+    state = rand_state(cfg, 2)
+    got, err = H.run_verify(cfg, H.Uploaded(w), H.t_f32(state), max_nodes=48)
+    assert err == tl.TL_EBADTREE
+    assert np.isnan(got).all()
+
+
+def test_slot_out_of_range_is_reported():
+    cfg, parents, paths = _error_case("production", {})
+    w = custom(cfg, parents, paths)
+    state = rand_state(cfg, 4)
+    slot = H.t_int([2, 4, 0])            # 4 is past the last of the 4 slots
+    got, err = H.run_verify(cfg, H.Uploaded(w), H.t_f32(state), slot=slot, num_slots=4)
+    assert err == tl.TL_EINVAL
+    assert np.isnan(got[rows_of(w, [1])]).all()
+    good = [0, 2]
+    ref = o_verify(cfg, sub(w, good), state, slot=np.array([2, 0]))
+    assert H.slice_rel_err(got[rows_of(w, good)], ref, sub(w, good).node_offsets) <= H.TOL
+
+
+# ----------------------------------------------------------------------------
+# empty paths and requests, slot indirection, determinism
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["production", "gdn", "large"])
+def test_empty_paths_and_empty_requests(name):
+    cfg = cfg_of(name, batch=4, prefix_len=0)
+    T = {"production": 64, "gdn": 100, "large": 200}[name]
+    parents = [topk(T, 1), np.zeros(0, np.int32), topk(T, 2), topk(T, 3)]
+    paths = [chain_path(parents[0], T - 1), [], [], chain_path(parents[3], 7)]
+    w = custom(cfg, parents, paths)
+    state = rand_state(cfg, 4)
+    up = H.Uploaded(w)
+    got, err = H.run_verify(cfg, up, H.t_f32(state))
+    assert err == 0
+    assert H.slice_rel_err(got, o_verify(cfg, w, state), w.node_offsets) <= H.TOL
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st) == 0
+    after = st.cpu().numpy()
+    np.testing.assert_array_equal(after[1], state[1])     # no nodes, no path
+    np.testing.assert_array_equal(after[2], state[2])     # empty path
+    assert H.state_rel_err(after, o_commit(cfg, w, state)) <= H.TOL
+
+
+def test_slot_indirection():
+    cfg = cfg_of("production", batch=3, prefix_len=0)
+    parents = [topk(64, s) for s in range(3)]
+    paths = [chain_path(p, 20) for p in parents]
+    w = custom(cfg, parents, paths)
+    state = rand_state(cfg, 5)
+    slot_np = np.array([4, 0, 2], np.int32)
+    up = H.Uploaded(w)
+    got, err = H.run_verify(cfg, up, H.t_f32(state), slot=H.t_int(slot_np), num_slots=5)
+    assert err == 0
+    assert H.slice_rel_err(got, o_verify(cfg, w, state, slot=slot_np), w.node_offsets) <= H.TOL
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st, slot=H.t_int(slot_np), num_slots=5) == 0
+    after = st.cpu().numpy()
+    ref = o_commit(cfg, w, state, slot=slot_np)
+    assert H.state_rel_err(after, ref) <= H.TOL
+    np.testing.assert_array_equal(after[[1, 3]], state[[1, 3]])   # slots no request names
+
+
+@pytest.mark.parametrize("name", ["production", "gdn", "large"])
+def test_deterministic(name):
+    cfg = cfg_of(name, prefix_len=0)
+    w = W.make(cfg, requests=[0, 1, 2])
+    state = rand_state(cfg, 3)
+    up = H.Uploaded(w)
+    a, _ = H.run_verify(cfg, up, H.t_f32(state))
+    b, _ = H.run_verify(cfg, up, H.t_f32(state))
+    np.testing.assert_array_equal(a, b)
+    s1, s2 = H.t_f32(state), H.t_f32(state)
+    H.run_commit(cfg, up, s1)
+    H.run_commit(cfg, up, s2)
+    np.testing.assert_array_equal(s1.cpu().numpy(), s2.cpu().numpy())
+
+
+# ----------------------------------------------------------------------------
+# several steps: verify, commit, next step's trees on the committed state
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name, reqs", [("large", [0, 1, 5]), ("gdn", [0, 1]), ("production", [0, 7])])
+def test_three_steps_with_carried_state(name, reqs):
+    cfg = cfg_of(name, prefix_len=0)
+    state = rand_state(cfg, len(reqs), scale=0.1)
+    st = H.t_f32(state)
+    ref_state = state.astype(np.float64)
+    for step in range(3):
+        w = W.make(cfg, step=step, requests=reqs)
+        up = H.Uploaded(w)
+        got, err = H.run_verify(cfg, up, st)
+        assert err == 0
+        ref = o_verify(cfg, w, ref_state)
+        e = H.slice_rel_err(got, ref, w.node_offsets)
+        assert e <= H.TOL, (step, e)
+        assert H.run_commit(cfg, up, st) == 0
+        ref_state = o_commit(cfg, w, ref_state)
+        e = H.state_rel_err(st.cpu().numpy(), ref_state)
+        assert e <= H.TOL, (step, e)
+
+
+# ----------------------------------------------------------------------------
+# shapes: head dimensions, group sizes, forests, the deepest tree, q scale
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("d", [16, 32, 64, 128])
+@pytest.mark.parametrize("hk, hv", [(2, 4), (3, 3), (1, 4)])
+@pytest.mark.parametrize("mode", [W.GLA, W.GDN])
+def test_head_dims_and_groups(d, hk, hv, mode):
+    cfg = cfg_of("production" if mode == W.GLA else "gdn", batch=3, num_qk_heads=hk, num_v_heads=hv,
+                 d_k=d, d_v=d, prefix_len=0, max_nodes=64)
+    parents = [topk(64, 1), topk(37, 2), topk(16, 3)]
+    paths = [chain_path(p, len(p) - 1) for p in parents]
+    w = custom(cfg, parents, paths)
+    state = rand_state(cfg, 3)
+    up = H.Uploaded(w)
+    got, err = H.run_verify(cfg, up, H.t_f32(state))
+    assert err == 0
+    e = H.slice_rel_err(got, o_verify(cfg, w, state), w.node_offsets)
+    assert e <= H.TOL, e
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st) == 0
+    assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
+
+
+def _multi_root(T, roots, seed):
+    rng = np.random.default_rng([seed, 5])
+    p = np.empty(T, np.int32)
+    p[:roots] = -1
+    for i in range(roots, T):
+        p[i] = rng.integers(0, i)
+    return p
+
+
+@pytest.mark.parametrize("name, T", [("production", 40), ("production", 64), ("gdn", 128),
+                                     ("large", 256), ("tiny", 12)])
+def test_forests_with_several_roots(name, T):
+    cfg = cfg_of(name, batch=2, prefix_len=0, max_nodes=max(T, W.CONFIGS[name].max_nodes))
+    parents = [_multi_root(T, 3, 1), _multi_root(T, 5, 2)]
+    paths = [chain_path(parents[0], T - 1), chain_path(parents[1], T // 2)]
+    w = custom(cfg, parents, paths)
+    state = rand_state(cfg, 2)
+    up = H.Uploaded(w)
+    got, err = H.run_verify(cfg, up, H.t_f32(state))
+    assert err == 0
+    assert H.slice_rel_err(got, o_verify(cfg, w, state), w.node_offsets) <= H.TOL
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st) == 0
+    assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
+
+
+@pytest.mark.parametrize("name", ["large", "gdn"])
+def test_deepest_tree_256_chain(name):
+    cfg = cfg_of(name, batch=1, prefix_len=0, max_nodes=256)
+    parent = W.chain_tree(256)
+    w = custom(cfg, [parent], [list(range(256))])
+    state = rand_state(cfg, 1, scale=0.1)
+    up = H.Uploaded(w)
+    got, err = H.run_verify(cfg, up, H.t_f32(state))
+    assert err == 0
+    assert H.slice_rel_err(got, o_verify(cfg, w, state), w.node_offsets) <= H.TOL
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st) == 0
+    assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
+
+
+@pytest.mark.parametrize("name", ["production", "gdn", "large", "tiny"])
+def test_query_scale(name):
+    cfg = cfg_of(name, prefix_len=0, q_scale=0.0883883)
+    w = W.make(cfg, requests=[0, 1])
+    state = rand_state(cfg, 2)
+    got, err = H.run_verify(cfg, H.Uploaded(w), H.t_f32(state))
+    assert err == 0
+    assert H.slice_rel_err(got, o_verify(cfg, w, state), w.node_offsets) <= H.TOL
+
+
+# ----------------------------------------------------------------------------
+# the full production batch, in the launch configuration bench.py times
+# ----------------------------------------------------------------------------
+
+def test_full_production_batch_sampled():
+    """All 32 requests go through one launch of each kernel; the oracle
+    checks sampled requests one by one (their S_pre from the oracle's own
+    prefix recurrence; the other requests get random states)."""
+    cfg = W.CONFIGS["production"]
+    w = W.make(cfg)
+    sample = [0, 13, 31]
+    state = rand_state(cfg, cfg.batch, scale=0.5)
+    state[sample] = H.oracle_prefix_state(cfg, 0, sample)
+    up = H.Uploaded(w)
+    got, err = H.run_verify(cfg, up, H.t_f32(state))
+    assert err == 0
+    assert np.isfinite(got).all()
+    ws = sub(w, sample)
+    e = H.slice_rel_err(got[rows_of(w, sample)], o_verify(cfg, ws, state[sample]), ws.node_offsets)
+    print(f"full batch, sampled verify max slice rel err {e:.3e}")
+    assert e <= H.TOL
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st) == 0
+    e = H.state_rel_err(st.cpu().numpy()[sample], o_commit(cfg, ws, state[sample]))
+    print(f"full batch, sampled commit max slot rel err {e:.3e}")
+    assert e <= H.TOL
