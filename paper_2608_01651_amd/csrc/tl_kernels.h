@@ -56,6 +56,8 @@ struct TopoArgs {
 };
 
 tl_status launch_verify(const tl_problem& p, const VerifyArgs& a, hipStream_t stream);
+tl_status launch_verify_tiled(const tl_problem& p, const VerifyArgs& a, hipStream_t stream);
+int verify_tiled_lds_bytes(int mode, int d, int tm, int W);
 tl_status launch_commit(const tl_problem& p, const CommitArgs& a, hipStream_t stream);
 tl_status launch_topology(const TopoArgs& a, hipStream_t stream);
 int verify_lds_bytes(const tl_problem& p, int tm);

@@ -35,8 +35,11 @@
 // steps with vector ALU products.
 //
 // Files: verify_gla_small.h (gated linear attention on MFMA, trees of <= 64
-// nodes), verify_gla.h (the same for larger trees), verify_gdn.h (delta
-// rule on MFMA), verify_vector.h (vector path), verify_common.h (layouts).
+// nodes), verify_tiled.hip (its own kernel: gated linear attention over
+// larger trees and the delta rule, node tile by node tile), verify_gla.h and
+// verify_gdn.h (the earlier per-wave MFMA paths, still used for shapes the
+// tiled kernel does not fit in LDS), verify_vector.h (vector path),
+// verify_common.h (layouts).
 #include <hip/hip_runtime.h>
 
 #include "tl_device.h"
@@ -167,6 +170,16 @@ static tl_status dispatch_d(int d, const VerifyArgs& a, hipStream_t stream) {
 }
 
 tl_status launch_verify(const tl_problem& p, const VerifyArgs& a, hipStream_t stream) {
+  // bf16 inputs, d >= 32: gated linear attention over trees of more than 64
+  // nodes, and the delta rule wherever its tile-sequential layout fits in
+  // LDS (trees of up to 128 nodes at d = 128), run node tile by node tile
+  // (verify_tiled.hip)
+  if (p.in_dtype == TL_BF16 && p.d_k >= 32) {
+    const int W = a.tm > 128 ? 4 : (a.tm > 64 ? 2 : 1);
+    if (p.mode == TL_MODE_GLA ? a.tm > 64
+                              : verify_tiled_lds_bytes(p.mode, p.d_k, a.tm, W) <= 160 * 1024)
+      return launch_verify_tiled(p, a, stream);
+  }
   if (p.mode == TL_MODE_GLA)
     return p.in_dtype == TL_F32 ? dispatch_d<TL_MODE_GLA, true>(p.d_k, a, stream)
                                 : dispatch_d<TL_MODE_GLA, false>(p.d_k, a, stream);
