@@ -128,6 +128,60 @@ tl_status tree_state_commit(const tl_problem* problem,
                             float* state, const int32_t* slot,
                             int32_t* dev_err, void* stream);
 
+/* One recurrent layer's inputs to tree_state_commit_layers: the same rows and
+ * layouts as tree_state_commit's k, v, g, beta and state (device pointers;
+ * beta NULL for TL_MODE_GLA, non-NULL for TL_MODE_GDN). */
+typedef struct tl_layer {
+  const void* k;      /* [N, Hk, d_k] */
+  const void* v;      /* [N, Hv, d_v] */
+  const float* g;     /* [N, Hv] */
+  const float* beta;  /* [N, Hv] or NULL */
+  float* state;       /* [num_slots, Hv, d_v, d_k], updated in place */
+} tl_layer;
+
+/* Most layers one tree_state_commit_layers call takes. */
+#define TL_MAX_COMMIT_LAYERS 64
+
+/* Unified cross-layer commit (§5.3 "Unified cross-layer state commit", with
+ * §4.4 Eq. accepted-commit per layer).
+ *
+ * The accepted path is shared by every recurrent layer, so the commits of
+ * num_layers layers (0 .. TL_MAX_COMMIT_LAYERS; 0 does nothing) are enqueued
+ * by one call: as one launch while a layer's B * Hv slots are fewer than the
+ * GPU holds at once, else as one launch per layer (a layer that fills the
+ * GPU on its own streams faster alone).  The path
+ * of request b is given by its sampled terminal node: terminal[b] is a
+ * request-local node index, or -1 when no draft token was accepted (every
+ * layer's slot keeps S_pre).  The path is that node and its ancestors, root
+ * first, and each layer's slot is updated exactly as tree_state_commit
+ * would update it with that path (bit-identical results).  `layers` is a
+ * HOST array of num_layers entries, read before the call returns; all
+ * layers share the forest, the slot map and the problem's shape.  Layers
+ * naming the same state memory race.
+ * Device errors: TL_EBADTREE (forest), TL_EBADPATH (terminal < -1 or >= T_b),
+ * TL_EINVAL (slot index). */
+tl_status tree_state_commit_layers(const tl_problem* problem, int32_t num_layers,
+                                   const tl_layer* layers,
+                                   const int32_t* node_offsets, const int32_t* parent,
+                                   const int32_t* terminal, /* [B] */
+                                   const int32_t* slot, int32_t* dev_err, void* stream);
+
+/* Device path compaction (§5.3): the accepted path of every request from its
+ * sampled terminal node, for consumers that need the accepted rows (e.g. the
+ * attention layers' cache commit, or tree_state_commit's path argument after
+ * a prefix sum of path_len).  Writes path_len[b] (0 when terminal[b] == -1)
+ * and the path's request-local nodes, root first, at
+ * path[node_offsets[b] + t] for t < path_len[b]; the request's other entries
+ * of `path` are left as they are.  Device errors: TL_EBADTREE (forest),
+ * TL_EBADPATH (terminal < -1 or >= T_b); nothing of that request is
+ * written. */
+tl_status tree_accepted_path(const tl_problem* problem,
+                             const int32_t* node_offsets, const int32_t* parent,
+                             const int32_t* terminal, /* [B] */
+                             int32_t* path_len,       /* [B] */
+                             int32_t* path,           /* [N] */
+                             int32_t* dev_err, void* stream);
+
 /* Tree topology of §4.1's notation table, as the kernels build it:
  * anc_mask[r, w] (W = ceil(max_nodes/64) uint64 words per node) has bit
  * (j mod 64) of word j/64 set iff local node j is r's node itself or one of

@@ -7,5 +7,5 @@ from .tree_oracle import (  # noqa: F401
     GLA, GDN, BF16, F32, MAX_NODES_LIMIT, SUPPORTED_D,
     OracleError, InvalidArg, BadTree, BadPath, Unsupported,
     check_problem, check_forest, check_paths, root_path, topology, step,
-    verify, commit, prefix_state,
+    verify, commit, prefix_state, accepted_paths, commit_layers,
 )

@@ -263,6 +263,44 @@ def commit(mode, num_qk_heads, node_offsets, parent, path_offsets, path, k, v,
     return new
 
 
+def accepted_paths(node_offsets, parent, terminal, max_nodes=MAX_NODES_LIMIT):
+    """Accepted path of every request from its sampled terminal node (§4.4:
+    P(a) = Anc(a) u {a}, listed root first; §5.3: one path descriptor per
+    request).  terminal[b] is request-local; -1 means nothing was accepted
+    (an empty path).  Raises BadTree for a malformed forest and BadPath for a
+    terminal outside [-1, T_b).  Returns (path_offsets, path) in the packed
+    form that commit() takes."""
+    check_forest(node_offsets, parent, max_nodes)
+    node_offsets = np.asarray(node_offsets, dtype=np.int64)
+    parent = np.asarray(parent, dtype=np.int64)
+    B = node_offsets.size - 1
+    if len(terminal) != B:
+        raise InvalidArg("terminal must have one entry per request")
+    offs = [0]
+    flat = []
+    for b in range(B):
+        T = int(node_offsets[b + 1] - node_offsets[b])
+        a = int(terminal[b])
+        if not (-1 <= a < T):
+            raise BadPath(f"request {b}: terminal {a} outside [-1,{T})")
+        p = [] if a == -1 else root_path(parent[node_offsets[b]:node_offsets[b + 1]], a)
+        flat.extend(p)
+        offs.append(len(flat))
+    return np.asarray(offs, dtype=np.int64), np.asarray(flat, dtype=np.int64)
+
+
+def commit_layers(mode, num_qk_heads, node_offsets, parent, terminal, layers,
+                  slot=None, max_nodes=MAX_NODES_LIMIT):
+    """Unified cross-layer commit (§5.3): every recurrent layer commits the same
+    accepted path, the one ending at terminal[b].  layers is a list of
+    (k, v, g, beta, state) per layer; returns the list of new states, each
+    exactly commit() of that layer over accepted_paths()."""
+    path_offsets, path = accepted_paths(node_offsets, parent, terminal, max_nodes)
+    return [commit(mode, num_qk_heads, node_offsets, parent, path_offsets, path,
+                   k, v, g, beta, state, slot=slot, max_nodes=max_nodes)
+            for (k, v, g, beta, state) in layers]
+
+
 def prefix_state(mode, k, v, g, beta, St0=None):
     """State after running the recurrence along a plain token sequence (a
     chain), starting from St0 (zeros if None).  Used to build S_pre from a

@@ -46,6 +46,22 @@ tl_status check_tensors(const tl_problem* p, const int32_t* node_offsets, const 
   return TL_OK;
 }
 
+void fill_common(const tl_problem* p, const int32_t* node_offsets, const int32_t* parent,
+                 const int32_t* slot, int32_t* dev_err, tl::CommitCommon& c) {
+  c.node_offsets = node_offsets;
+  c.parent = parent;
+  c.slot = slot;
+  c.dev_err = dev_err;
+  c.batch = p->batch;
+  c.Hk = p->num_qk_heads;
+  c.Hv = p->num_v_heads;
+  c.max_nodes = p->max_nodes;
+  c.num_slots = p->num_slots;
+#ifdef TL_TRACE
+  c.trace = g_trace;
+#endif
+}
+
 }  // namespace
 
 extern "C" {
@@ -104,26 +120,58 @@ tl_status tree_state_commit(const tl_problem* problem, const int32_t* node_offse
   if (path && !aligned(path, 4)) return TL_EINVAL;
   if (dev_err && !aligned(dev_err, 4)) return TL_EINVAL;
   tl::CommitArgs a;
-  a.node_offsets = node_offsets;
-  a.parent = parent;
+  fill_common(problem, node_offsets, parent, slot, dev_err, a.c);
+  a.ly = tl::CommitLayer{k, v, g, beta, state};
   a.path_offsets = path_offsets;
   a.path = path;   // NULL is allowed when every path is empty
-  a.k = k;
-  a.v = v;
-  a.g = g;
-  a.beta = beta;
-  a.state = state;
-  a.slot = slot;
+  return tl::launch_commit(*problem, a, reinterpret_cast<hipStream_t>(stream));
+}
+
+tl_status tree_state_commit_layers(const tl_problem* problem, int32_t num_layers,
+                                   const tl_layer* layers, const int32_t* node_offsets,
+                                   const int32_t* parent, const int32_t* terminal,
+                                   const int32_t* slot, int32_t* dev_err, void* stream) {
+  tl_status st = check_problem(problem);
+  if (st != TL_OK) return st;
+  if (num_layers < 0 || num_layers > TL_MAX_COMMIT_LAYERS) return TL_EINVAL;
+  if (problem->batch == 0 || num_layers == 0) return TL_OK;
+  if (!layers || !terminal || !aligned(terminal, 4)) return TL_EINVAL;
+  if (dev_err && !aligned(dev_err, 4)) return TL_EINVAL;
+  tl::CommitLayersArgs a;
+  fill_common(problem, node_offsets, parent, slot, dev_err, a.c);
+  a.terminal = terminal;
+  a.num_layers = num_layers;
+  for (int l = 0; l < num_layers; ++l) {
+    const tl_layer& L = layers[l];
+    st = check_tensors(problem, node_offsets, parent, L.k, L.v, L.g, L.beta, L.state, slot);
+    if (st != TL_OK) return st;
+    a.ly[l] = tl::CommitLayer{L.k, L.v, L.g, L.beta, L.state};
+  }
+  for (int l = num_layers; l < tl::kMaxCommitLayers; ++l) a.ly[l] = tl::CommitLayer{};
+  return tl::launch_commit_layers(*problem, a, reinterpret_cast<hipStream_t>(stream));
+}
+
+tl_status tree_accepted_path(const tl_problem* problem, const int32_t* node_offsets,
+                             const int32_t* parent, const int32_t* terminal, int32_t* path_len,
+                             int32_t* path, int32_t* dev_err, void* stream) {
+  tl_status st = check_problem(problem);
+  if (st != TL_OK) return st;
+  if (problem->batch == 0) return TL_OK;
+  if (!node_offsets || !parent || !terminal || !path_len || !path) return TL_EINVAL;
+  if (!aligned(node_offsets, 4) || !aligned(parent, 4) || !aligned(terminal, 4) ||
+      !aligned(path_len, 4) || !aligned(path, 4))
+    return TL_EINVAL;
+  if (dev_err && !aligned(dev_err, 4)) return TL_EINVAL;
+  tl::PathArgs a;
+  a.node_offsets = node_offsets;
+  a.parent = parent;
+  a.terminal = terminal;
+  a.path_len = path_len;
+  a.path = path;
   a.dev_err = dev_err;
   a.batch = problem->batch;
-  a.Hk = problem->num_qk_heads;
-  a.Hv = problem->num_v_heads;
   a.max_nodes = problem->max_nodes;
-  a.num_slots = problem->num_slots;
-#ifdef TL_TRACE
-  a.trace = g_trace;
-#endif
-  return tl::launch_commit(*problem, a, reinterpret_cast<hipStream_t>(stream));
+  return tl::launch_accepted_path(a, reinterpret_cast<hipStream_t>(stream));
 }
 
 tl_status tree_topology_export(const tl_problem* problem, const int32_t* node_offsets,

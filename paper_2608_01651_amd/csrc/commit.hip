@@ -1,4 +1,4 @@
-// Accepted-path commit (§4.4, Eq. accepted-commit).
+// Accepted-path commit (§4.4, Eq. accepted-commit), one layer or many.
 //
 // S_new = P_a S_pre + (D_a K_a)^T U_a is, by Lemma 1, the post-update state
 // of the terminal node a, i.e. the recurrence replayed along the accepted
@@ -12,6 +12,13 @@
 // path before it writes anything, and every block is read before it is
 // written; an empty path leaves the slot untouched.  The state is read and
 // written once, with non-temporal loads and stores.
+//
+// The accepted path is shared by every recurrent layer, so §5.3 folds the
+// commits of all layers into one launch; commit_layers_kernel does that, one
+// workgroup per (layer, request, v-head).  There the path arrives as the
+// sampled terminal node of each request (the path descriptor of §5.3) and is
+// rebuilt on chip by walking the parents from it; accepted_path_kernel
+// exports the same lists.
 #include <hip/hip_runtime.h>
 
 #include "tl_device.h"
@@ -30,12 +37,51 @@ struct CommitShape {
   static constexpr int PASSES = (ROWS + RPP - 1) / RPP;
 };
 
-// One workgroup per (request, v-head) slot.  The path is validated and its
-// rows (k, v, gates) are staged in LDS once; the slot is then replayed and
-// stored in blocks of ROWS rows, whose loads are all issued at the start
-// (delta rule: two blocks at a time).
-template <int MODE, int D, bool F32IN>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void commit_kernel(CommitArgs a) {
+// Block-wide OR through LDS: each wave's ballot goes to s_red[wave] (one
+// array per use).  The barrier waits for LDS traffic only, so the state
+// loads in flight stay in flight.
+__device__ inline bool block_or_lds(bool pred, int* s_red) {
+  const bool any = __ballot(pred) != 0ull;
+  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = any ? 1 : 0;
+  lds_barrier();
+  int r = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) r |= s_red[w];
+  return r != 0;
+}
+
+// Accepted path ending at `term` (0 <= term < T) of a checked forest whose
+// parents are in s_par: every thread walks the same root path (broadcast
+// LDS reads; parents precede children, so the walk ends within T steps), and
+// thread s keeps the node s steps above the terminal, which is path entry
+// L - 1 - s.  Writes s_path[0 .. L) root first and returns L (uniform).
+__device__ inline int path_to_root(int term, const int* s_par, int* s_path) {
+  const int tid = threadIdx.x;
+  int j = term, s = 0, mine = -1;
+  while (j >= 0) {
+    if (s == tid) mine = j;
+    j = s_par[j];
+    ++s;
+  }
+  if (tid < s) s_path[s - 1 - tid] = mine;
+  lds_barrier();
+  return s;
+}
+
+// Commit of one (request b, v-head h) slot of one layer.  TERMINAL: the path
+// is the one ending at terminal[b] (-1: nothing accepted); otherwise it is
+// path[path_offsets[b] .. path_offsets[b+1]-1], checked link by link.
+//
+// Order of the memory traffic: the parents (and the listed path) are
+// requested first, then the state blocks, all unconditionally (a request
+// that commits nothing points its state loads at one line), so the checks
+// wait only for the former; the checks synchronise through LDS alone; the
+// gates and k/v rows of the path then go out in one round trip, and the
+// replay waits for everything.
+template <int MODE, int D, bool F32IN, bool TERMINAL>
+__device__ __attribute__((always_inline)) inline void commit_unit(
+    const CommitCommon& a, const CommitLayer& ly, const int32_t* path_offsets,
+    const int32_t* path, const int32_t* terminal, int b, int h) {
   using SH = CommitShape<D>;
   constexpr int ROWS = SH::ROWS, NRB = SH::NRB, LPR = SH::LPR, RPP = SH::RPP, PASSES = SH::PASSES;
   constexpr bool GDN = (MODE == TL_MODE_GDN);
@@ -43,42 +89,65 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   __shared__ __align__(16) float s_v[kCommitChunk * D];
   __shared__ float s_gam[kCommitChunk];
   __shared__ float s_beta[kCommitChunk];
-  __shared__ int s_row[kCommitChunk];
   __shared__ int s_par[kMaxNodes];
+  __shared__ int s_path[kMaxNodes];
+  __shared__ int s_red[2 * kWaves];
 
   const int tid = threadIdx.x;
   TL_TRACE_POINT(a, 0);
-  const int b = blockIdx.x / a.Hv, h = blockIdx.x % a.Hv;
   const int hq = h / (a.Hv / a.Hk);
 
   Request rq;
   if (!load_request(a.node_offsets, b, a.max_nodes, a.dev_err, rq)) return;
   const int T = rq.T, off = rq.off;
-  const int p0 = a.path_offsets[b], p1 = a.path_offsets[b + 1];
-  const int Lp = p1 - p0;
-  if (p0 < 0 || Lp < 0) {
-    if (tid == 0) report(a.dev_err, TL_EINVAL);
-    return;
+  int p0 = 0, Lp = 0, term = -1;
+  if constexpr (TERMINAL) {
+    term = terminal[b];
+  } else {
+    p0 = path_offsets[b];
+    Lp = path_offsets[b + 1] - p0;
+    if (p0 < 0 || Lp < 0) {
+      if (tid == 0) report(a.dev_err, TL_EINVAL);
+      return;
+    }
   }
   const int sidx = a.slot ? a.slot[b] : b;
   if (sidx < 0 || sidx >= a.num_slots) {
     if (tid == 0) report(a.dev_err, TL_EINVAL);
     return;
   }
+  if (T == 0) {   // an empty request accepts nothing
+    if ((TERMINAL ? term != -1 : Lp != 0) && tid == 0) report(a.dev_err, TL_EBADPATH);
+    return;
+  }
   TL_TRACE_POINT(a, 1);
 
-  // state blocks are read first so that their latency overlaps the checks
-  // below; nothing is written before they pass
-  float* Sp = a.state + ((size_t)sidx * a.Hv + h) * D * D;
+  // parents and listed path nodes (clamped to valid rows; lanes past the end
+  // are ignored)
+  const int par = a.parent[off + min(tid, T - 1)];
+  bool path_ok = true;
+  int node = -1;
+  if constexpr (!TERMINAL) {
+    path_ok = !(Lp > T || (Lp > 0 && path == nullptr));
+    const int32_t* np = (path_ok && Lp > 0) ? path + p0 + min(tid, Lp - 1) : a.parent + off;
+    node = *np;
+  }
+
+  // state blocks; `keep` zeroes the offsets of a slot that is not written
+  // (an AND with a value the compiler cannot see through, so the loads stay
+  // one straight-line sequence)
+  const bool need = TERMINAL ? term >= 0 : Lp > 0;
+  float* Sp = ly.state + ((size_t)sidx * a.Hv + h) * D * D;
   const int col = (tid % LPR) * 4;
   const int rsub = tid / LPR;
+  uint32_t keep = need ? 0xffffffffu : 0u;
+  asm volatile("" : "+v"(keep));
   auto load_block = [&](int rb, f32x4 (&st)[PASSES]) {
 #pragma unroll
     for (int p = 0; p < PASSES; ++p) {
-      const int row = p * RPP + rsub;
-      if (row < ROWS)
-        st[p] = __builtin_nontemporal_load(
-            reinterpret_cast<const f32x4*>(Sp + (size_t)(rb * ROWS + row) * D + col));
+      const int row = min(p * RPP + rsub, ROWS - 1);
+      const uint32_t o = (uint32_t)((rb * ROWS + row) * D + col) & keep;
+      st[p] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(Sp + o));
     }
   };
   auto store_block = [&](int rb, const f32x4 (&st)[PASSES]) {
@@ -94,54 +163,52 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   // row reductions and streams the blocks through two buffers
   constexpr int NBUF = GDN ? (NRB < 2 ? NRB : 2) : NRB;
   f32x4 sb[NBUF][PASSES];
-  if (Lp > 0) {
 #pragma unroll
-    for (int rb = 0; rb < NBUF; ++rb) load_block(rb, sb[rb]);
-  }
+  for (int rb = 0; rb < NBUF; ++rb) load_block(rb, sb[rb]);
 
-  // forest of request b (one node per thread) and the path, loaded together;
-  // the path's links are then checked against the parents in LDS
-  int par = -1, node = -1;
-  if (tid < T) par = a.parent[off + tid];
-  const bool path_ok = !(Lp > T || (Lp > 0 && a.path == nullptr));
-  if (path_ok && tid < Lp) node = a.path[p0 + tid];
+  // checks, through LDS only
   if (tid < T) s_par[tid] = par;
-  const bool bad_tree = (tid < T) && !(par == -1 || (par >= 0 && par < tid));
-  const bool node_in = node >= 0 && node < T;
+  if (!TERMINAL && tid < Lp && tid < kMaxNodes) s_path[tid] = node;
+  const bool bad_tree = tid < T && !(par == -1 || (par >= 0 && par < tid));
   TL_TRACE_POINT(a, 2);
-  if (__syncthreads_or(bad_tree)) {
+  if (block_or_lds(bad_tree, s_red)) {
     if (tid == 0) report(a.dev_err, TL_EBADTREE);
     return;
   }
-  {
-    bool bad = !path_ok;
-    if (!bad && tid < Lp) {
-      const int want = (tid == 0) ? -1 : a.path[p0 + tid - 1];
-      bad = !node_in || s_par[node] != want;
-    }
-    if (__syncthreads_or(bad)) {
+  if constexpr (TERMINAL) {
+    if (term < -1 || term >= T) {
       if (tid == 0) report(a.dev_err, TL_EBADPATH);
       return;
     }
+    if (term < 0) return;
+    Lp = path_to_root(term, s_par, s_path);
+  } else {
+    bool bad = !path_ok;
+    if (!bad && tid < Lp) {
+      const bool node_in = node >= 0 && node < T;
+      bad = !node_in || s_par[node] != (tid == 0 ? -1 : s_path[tid - 1]);
+    }
+    if (block_or_lds(bad, s_red + kWaves)) {
+      if (tid == 0) report(a.dev_err, TL_EBADPATH);
+      return;
+    }
+    if (Lp == 0) return;
   }
-  if (Lp == 0) return;
   TL_TRACE_POINT(a, 3);
 
   const size_t qk_row = (size_t)a.Hk * D, v_row = (size_t)a.Hv * D;
-  // stage path steps [c0, c0 + n): row ids and gates, then k and v rows
+  // stage path steps [c0, c0 + n): gates, k and v rows, in one round trip
   auto stage = [&](int c0, int n) {
     if (tid < n) {
-      const int r = off + a.path[p0 + c0 + tid];
-      s_row[tid] = r;
-      s_gam[tid] = __expf(a.g[(size_t)r * a.Hv + h]);
-      if constexpr (GDN) s_beta[tid] = a.beta[(size_t)r * a.Hv + h];
+      const size_t r = (size_t)(off + s_path[c0 + tid]);
+      s_gam[tid] = __expf(ly.g[r * a.Hv + h]);
+      if constexpr (GDN) s_beta[tid] = ly.beta[r * a.Hv + h];
     }
-    __syncthreads();
     for (int x = tid * 4; x < n * D; x += kThreads * 4) {
       const int t = x / D, e = x % D;
-      const size_t r = (size_t)s_row[t];
-      *reinterpret_cast<f32x4*>(s_k + x) = load4<F32IN>(a.k, r * qk_row + (size_t)hq * D + e);
-      *reinterpret_cast<f32x4*>(s_v + x) = load4<F32IN>(a.v, r * v_row + (size_t)h * D + e);
+      const size_t r = (size_t)(off + s_path[c0 + t]);
+      *reinterpret_cast<f32x4*>(s_k + x) = load4<F32IN>(ly.k, r * qk_row + (size_t)hq * D + e);
+      *reinterpret_cast<f32x4*>(s_v + x) = load4<F32IN>(ly.v, r * v_row + (size_t)h * D + e);
     }
     __syncthreads();
   };
@@ -167,6 +234,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     }
   };
 
+  // with the whole slot in registers, the path rows are requested only once
+  // the slot has arrived: scattered row reads issued into the middle of the
+  // launch-wide state stream slowed it down
+  if constexpr (NBUF == NRB) wait_vmem();
   if (Lp <= kCommitChunk) {
     stage(0, Lp);
     TL_TRACE_POINT(a, 4);
@@ -193,9 +264,60 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
   TL_TRACE_POINT(a, 5);
 }
 
+// One workgroup per (request, v-head) slot of one layer.
+template <int MODE, int D, bool F32IN>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void commit_kernel(CommitArgs a) {
+  commit_unit<MODE, D, F32IN, false>(a.c, a.ly, a.path_offsets, a.path, nullptr, blockIdx.x / a.c.Hv,
+                                     blockIdx.x % a.c.Hv);
+}
+
+// One workgroup per (layer, request, v-head) slot; consecutive workgroups
+// walk the v-heads, then the requests, then the layers.
+template <int MODE, int D, bool F32IN, int NL>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void commit_layers_kernel(
+    CommitLayersArgsN<NL> a) {
+  const int per_layer = a.c.batch * a.c.Hv;
+  const int layer = blockIdx.x / per_layer, rem = blockIdx.x % per_layer;
+  commit_unit<MODE, D, F32IN, true>(a.c, a.ly[layer], nullptr, nullptr, a.terminal, rem / a.c.Hv,
+                                    rem % a.c.Hv);
+}
+
+// Accepted path of every request from its terminal node: path_len[b] and the
+// path's request-local nodes, root first, at path[node_offsets[b] + t].  One
+// workgroup per request.
+__global__ __launch_bounds__(kThreads) void accepted_path_kernel(PathArgs a) {
+  __shared__ int s_par[kMaxNodes];
+  __shared__ int s_path[kMaxNodes];
+  __shared__ int s_red[kWaves];
+  const int tid = threadIdx.x, b = blockIdx.x;
+  Request rq;
+  if (!load_request(a.node_offsets, b, a.max_nodes, a.dev_err, rq)) return;
+  const int T = rq.T, term = a.terminal[b];
+  if (T == 0) {
+    if (tid == 0) {
+      if (term == -1) a.path_len[b] = 0;
+      else report(a.dev_err, TL_EBADPATH);
+    }
+    return;
+  }
+  const int par = a.parent[rq.off + min(tid, T - 1)];
+  if (tid < T) s_par[tid] = par;
+  if (block_or_lds(tid < T && !(par == -1 || (par >= 0 && par < tid)), s_red)) {
+    if (tid == 0) report(a.dev_err, TL_EBADTREE);
+    return;
+  }
+  if (term < -1 || term >= T) {
+    if (tid == 0) report(a.dev_err, TL_EBADPATH);
+    return;
+  }
+  const int L = term < 0 ? 0 : path_to_root(term, s_par, s_path);
+  if (tid == 0) a.path_len[b] = L;
+  if (tid < L) a.path[rq.off + tid] = s_path[tid];
+}
+
 template <int MODE, int D, bool F32IN>
 static tl_status launch_one(const CommitArgs& a, hipStream_t stream) {
-  const long blocks = (long)a.batch * a.Hv;
+  const long blocks = (long)a.c.batch * a.c.Hv;
   if (blocks == 0) return TL_OK;
   if (blocks > 0x7fffffffL) return TL_EINVAL;
   hipLaunchKernelGGL((commit_kernel<MODE, D, F32IN>), dim3((unsigned)blocks), dim3(kThreads), 0,
@@ -203,8 +325,18 @@ static tl_status launch_one(const CommitArgs& a, hipStream_t stream) {
   return hipGetLastError() == hipSuccess ? TL_OK : TL_EHIP;
 }
 
-template <int MODE, bool F32IN>
-static tl_status dispatch_d(int d, const CommitArgs& a, hipStream_t stream) {
+template <int MODE, int D, bool F32IN, int NL>
+static tl_status launch_one(const CommitLayersArgsN<NL>& a, hipStream_t stream) {
+  const long blocks = (long)a.num_layers * a.c.batch * a.c.Hv;
+  if (blocks == 0) return TL_OK;
+  if (blocks > 0x7fffffffL) return TL_EINVAL;
+  hipLaunchKernelGGL((commit_layers_kernel<MODE, D, F32IN, NL>), dim3((unsigned)blocks), dim3(kThreads),
+                     0, stream, a);
+  return hipGetLastError() == hipSuccess ? TL_OK : TL_EHIP;
+}
+
+template <int MODE, bool F32IN, class Args>
+static tl_status dispatch_d(int d, const Args& a, hipStream_t stream) {
   switch (d) {
     case 16: return launch_one<MODE, 16, F32IN>(a, stream);
     case 32: return launch_one<MODE, 32, F32IN>(a, stream);
@@ -214,12 +346,53 @@ static tl_status dispatch_d(int d, const CommitArgs& a, hipStream_t stream) {
   }
 }
 
-tl_status launch_commit(const tl_problem& p, const CommitArgs& a, hipStream_t stream) {
+template <class Args>
+static tl_status dispatch(const tl_problem& p, const Args& a, hipStream_t stream) {
   if (p.mode == TL_MODE_GLA)
     return p.in_dtype == TL_F32 ? dispatch_d<TL_MODE_GLA, true>(p.d_k, a, stream)
                                 : dispatch_d<TL_MODE_GLA, false>(p.d_k, a, stream);
   return p.in_dtype == TL_F32 ? dispatch_d<TL_MODE_GDN, true>(p.d_k, a, stream)
                               : dispatch_d<TL_MODE_GDN, false>(p.d_k, a, stream);
+}
+
+tl_status launch_commit(const tl_problem& p, const CommitArgs& a, hipStream_t stream) {
+  return dispatch(p, a, stream);
+}
+
+// Workgroups of the commit kernels that one GPU holds at once (four per
+// compute unit: 128 registers and 35 KB of LDS each).
+static long resident_commit_blocks() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  return 4L * cus;
+}
+
+// A layer whose slots alone fill the GPU goes out as a launch of its own:
+// each launch then reads its states and writes them back in two broad
+// phases, which on HBM3E outran one launch in which layers overlap and reads
+// and writes mix.  Smaller layers share one launch, which keeps the GPU full.
+tl_status launch_commit_layers(const tl_problem& p, const CommitLayersArgs& a, hipStream_t stream) {
+  const long per_layer = (long)a.c.batch * a.c.Hv;
+  const long resident = resident_commit_blocks();
+  if (a.num_layers == 1 || resident == 0 || per_layer < resident) return dispatch(p, a, stream);
+  CommitLayersArgsN<1> one;
+  one.c = a.c;
+  one.terminal = a.terminal;
+  one.num_layers = 1;
+  for (int l = 0; l < a.num_layers; ++l) {
+    one.ly[0] = a.ly[l];
+    const tl_status st = dispatch(p, one, stream);
+    if (st != TL_OK) return st;
+  }
+  return TL_OK;
+}
+
+tl_status launch_accepted_path(const PathArgs& a, hipStream_t stream) {
+  if (a.batch == 0) return TL_OK;
+  hipLaunchKernelGGL(accepted_path_kernel, dim3((unsigned)a.batch), dim3(kThreads), 0, stream, a);
+  return hipGetLastError() == hipSuccess ? TL_OK : TL_EHIP;
 }
 
 }  // namespace tl

@@ -268,6 +268,14 @@ __device__ inline void wait_vmem_below() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// Output rows are written once and never read back by the kernel; NT
+// selects the non-temporal (streaming) cache policy for them.
+template <bool NT>
+__device__ inline void store_out(float* p, const f32x4& v) {
+  if constexpr (NT) __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(p));
+  else *reinterpret_cast<f32x4*>(p) = v;
+}
+
 // Workgroup barrier for LDS data: this wave's LDS accesses complete, then
 // s_barrier.  Unlike __syncthreads() it does not wait for the wave's
 // outstanding global loads, so loads issued for later phases stay in flight.

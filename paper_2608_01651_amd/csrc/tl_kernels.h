@@ -28,22 +28,58 @@ struct VerifyArgs {
 #endif
 };
 
-struct CommitArgs {
+// What every commit launch shares: the forest, the slot map and the shape.
+struct CommitCommon {
   const int32_t* node_offsets;
   const int32_t* parent;
-  const int32_t* path_offsets;
-  const int32_t* path;
-  const void* k;
-  const void* v;
-  const float* g;
-  const float* beta;
-  float* state;
   const int32_t* slot;
   int32_t* dev_err;
   int batch, Hk, Hv, max_nodes, num_slots;
 #ifdef TL_TRACE
   long long* trace;  // [blocks][16] wall-clock stamps (trace builds only)
 #endif
+};
+
+// One layer's per-node rows and state slots.
+struct CommitLayer {
+  const void* k;
+  const void* v;
+  const float* g;
+  const float* beta;
+  float* state;
+};
+
+// tree_state_commit: one layer, explicit root-first paths.
+struct CommitArgs {
+  CommitCommon c;
+  CommitLayer ly;
+  const int32_t* path_offsets;
+  const int32_t* path;
+};
+
+// tree_state_commit_layers: up to kMaxCommitLayers layers in one launch, the
+// accepted path of each request given by its terminal node.
+// NL is the capacity of the layer table (the kernel argument's size): 1 for
+// the launches that serve a single layer.
+constexpr int kMaxCommitLayers = 64;
+template <int NL>
+struct CommitLayersArgsN {
+  CommitCommon c;
+  const int32_t* terminal;
+  int num_layers;
+  CommitLayer ly[NL];
+};
+using CommitLayersArgs = CommitLayersArgsN<kMaxCommitLayers>;
+
+// tree_accepted_path
+struct PathArgs {
+  const int32_t* node_offsets;
+  const int32_t* parent;
+  const int32_t* terminal;
+  int32_t* path_len;
+  int32_t* path;
+  int32_t* dev_err;
+  int batch, max_nodes;
 };
 
 struct TopoArgs {
@@ -59,6 +95,8 @@ tl_status launch_verify(const tl_problem& p, const VerifyArgs& a, hipStream_t st
 tl_status launch_verify_tiled(const tl_problem& p, const VerifyArgs& a, hipStream_t stream);
 int verify_tiled_lds_bytes(int mode, int d, int tm, int W);
 tl_status launch_commit(const tl_problem& p, const CommitArgs& a, hipStream_t stream);
+tl_status launch_commit_layers(const tl_problem& p, const CommitLayersArgs& a, hipStream_t stream);
+tl_status launch_accepted_path(const PathArgs& a, hipStream_t stream);
 tl_status launch_topology(const TopoArgs& a, hipStream_t stream);
 int verify_lds_bytes(const tl_problem& p, int tm);
 

@@ -486,7 +486,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
       v0 = v1;
       v1 = v2;
     }
-    if (vw && pend_row >= 0) *reinterpret_cast<f32x4*>(obase + (size_t)pend_row * v_row) = pend;
+    if (vw && pend_row >= 0) store_out<MODE == TL_MODE_GDN>(obase + (size_t)pend_row * v_row, pend);
     pend_row = -1;
     load_q(I + 2, q2);   // rows clamped: harmless past the last tile
     v2 = load_v(I + 2);
@@ -512,7 +512,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     }
     if (I < 2) TL_TRACE_POINT(a, 5 + I);
   }
-  if (vw && pend_row >= 0) *reinterpret_cast<f32x4*>(obase + (size_t)pend_row * v_row) = pend;
+  if (vw && pend_row >= 0) store_out<MODE == TL_MODE_GDN>(obase + (size_t)pend_row * v_row, pend);
   TL_TRACE_POINT(a, 15);
 }
 

@@ -42,6 +42,15 @@ class Problem(ctypes.Structure):
     ]
 
 
+class Layer(ctypes.Structure):
+    """tl_layer: one layer's k, v, g, beta and state device pointers."""
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("g", ctypes.c_void_p),
+                ("beta", ctypes.c_void_p), ("state", ctypes.c_void_p)]
+
+
+MAX_COMMIT_LAYERS = 64
+
+
 def problem(batch, num_qk_heads, num_v_heads, d_k, d_v, max_nodes, num_slots=None,
             mode=GLA, in_dtype=BF16, q_scale=1.0):
     return Problem(batch, num_qk_heads, num_v_heads, d_k, d_v, max_nodes,
@@ -65,6 +74,10 @@ def lib():
         L.tree_lin_attn_verify.restype = ctypes.c_int
         L.tree_state_commit.argtypes = [P] + [vp] * 12
         L.tree_state_commit.restype = ctypes.c_int
+        L.tree_state_commit_layers.argtypes = [P, ctypes.c_int32, ctypes.POINTER(Layer)] + [vp] * 6
+        L.tree_state_commit_layers.restype = ctypes.c_int
+        L.tree_accepted_path.argtypes = [P] + [vp] * 7
+        L.tree_accepted_path.restype = ctypes.c_int
         L.tree_topology_export.argtypes = [P] + [vp] * 6
         L.tree_topology_export.restype = ctypes.c_int
         L.tl_status_string.argtypes = [ctypes.c_int]
@@ -151,3 +164,33 @@ def topology(prob, node_offsets, parent, anc_mask, depth, dev_err=None, stream=N
         _ptr(anc_mask, "anc_mask", (torch.int64,)), _ptr(depth, "depth", _I32),
         _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
     _check(s, "tree_topology_export")
+
+
+def layer(k, v, g, beta, state):
+    """One entry of commit_layers' layer table (checks dtypes and layout)."""
+    return Layer(_ptr(k, "k", _IN), _ptr(v, "v", _IN), _ptr(g, "g", _F32),
+                 _ptr(beta, "beta", _F32, True), _ptr(state, "state", _F32))
+
+
+def commit_layers(prob, layers, node_offsets, parent, terminal, slot=None, dev_err=None,
+                  stream=None):
+    """tree_state_commit_layers: one launch commits every layer of `layers`
+    (a list of layer(...) entries or of (k, v, g, beta, state) tuples) along
+    the path that ends at terminal[b] (-1: nothing accepted)."""
+    table = [x if isinstance(x, Layer) else layer(*x) for x in layers]
+    arr = (Layer * max(1, len(table)))(*table)
+    s = lib().tree_state_commit_layers(
+        ctypes.byref(prob), len(table), arr, _ptr(node_offsets, "node_offsets", _I32),
+        _ptr(parent, "parent", _I32), _ptr(terminal, "terminal", _I32),
+        _ptr(slot, "slot", _I32, True), _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
+    _check(s, "tree_state_commit_layers")
+
+
+def accepted_path(prob, node_offsets, parent, terminal, path_len, path, dev_err=None,
+                  stream=None):
+    """tree_accepted_path: path_len [B] and the root-first paths at path[node_offsets[b] + t]."""
+    s = lib().tree_accepted_path(
+        ctypes.byref(prob), _ptr(node_offsets, "node_offsets", _I32), _ptr(parent, "parent", _I32),
+        _ptr(terminal, "terminal", _I32), _ptr(path_len, "path_len", _I32), _ptr(path, "path", _I32),
+        _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
+    _check(s, "tree_accepted_path")

@@ -33,6 +33,7 @@ def test_library_exports_every_declared_function():
     L = _lib_or_build()
     names = _declared_functions()
     assert {"tree_lin_attn_verify", "tree_state_commit", "tree_topology_export",
+            "tree_state_commit_layers", "tree_accepted_path",
             "tl_status_string", "tl_version"} <= set(names)
     for n in names:
         assert hasattr(L, n), f"{n} declared in include/treelin.h but not exported"
@@ -77,6 +78,26 @@ def _topology(prob, mask=A16, depth=A16):
         None if prob is None else ctypes.byref(prob), A16, A16, mask, depth, None, None)
 
 
+def _layers(prob, n, **kw):
+    beta = A16 if prob.mode == tl.GDN else None
+    f = dict(k=A16, v=A16, g=A16, beta=beta, state=A16)
+    f.update(kw)
+    return [tl.Layer(f["k"], f["v"], f["g"], f["beta"], f["state"]) for _ in range(n)]
+
+
+def _commit_layers(prob, n=2, layers=None, terminal=A16, offs=A16, par=A16):
+    table = _layers(prob, n) if layers is None and prob is not None else (layers or [])
+    arr = (tl.Layer * max(1, len(table)))(*table)
+    return _lib_or_build().tree_state_commit_layers(
+        None if prob is None else ctypes.byref(prob), n, arr if layers != "null" else None,
+        offs, par, terminal, None, None, None)
+
+
+def _accepted_path(prob, terminal=A16, path_len=A16, path=A16):
+    return _lib_or_build().tree_accepted_path(
+        None if prob is None else ctypes.byref(prob), A16, A16, terminal, path_len, path, None, None)
+
+
 def P(**kw):
     base = dict(batch=2, num_qk_heads=2, num_v_heads=4, d_k=64, d_v=64, max_nodes=64)
     base.update({k: v for k, v in kw.items() if k in base})
@@ -102,6 +123,8 @@ def test_problem_checks(prob, code):
     assert _verify(prob) == code
     assert _commit(prob) == code
     assert _topology(prob) == code
+    assert _commit_layers(prob) == code
+    assert _accepted_path(prob) == code
 
 
 def test_empty_batch_is_a_no_op():
@@ -140,3 +163,32 @@ def test_commit_and_topology_pointer_checks():
     assert _topology(P(), mask=None) == tl.TL_EINVAL
     assert _topology(P(), mask=A16 + 4) == tl.TL_EINVAL
     assert _topology(P(), depth=None) == tl.TL_EINVAL
+
+
+def test_commit_layers_checks():
+    L = _lib_or_build()
+    assert _commit_layers(P(), n=tl.MAX_COMMIT_LAYERS + 1,
+                          layers=_layers(P(), tl.MAX_COMMIT_LAYERS + 1)) == tl.TL_EINVAL
+    assert _commit_layers(P(), n=-1, layers=[]) == tl.TL_EINVAL
+    assert _commit_layers(P(), n=0, layers=[]) == tl.TL_OK            # nothing to do
+    assert _commit_layers(P(batch=0)) == tl.TL_OK
+    assert _commit_layers(P(), terminal=None) == tl.TL_EINVAL
+    assert _commit_layers(P(), terminal=MIS) == tl.TL_EINVAL
+    assert _commit_layers(P(), offs=None) == tl.TL_EINVAL
+    assert L.tree_state_commit_layers(ctypes.byref(P()), 2, None, A16, A16, A16,
+                                      None, None, None) == tl.TL_EINVAL
+    # one bad layer anywhere in the table fails the whole call
+    for field, val in (("state", None), ("k", None), ("v", MIS), ("state", MIS), ("g", None)):
+        table = _layers(P(), 3)
+        setattr(table[2], field, val)
+        assert _commit_layers(P(), n=3, layers=table) == tl.TL_EINVAL, field
+    assert _commit_layers(P(mode=tl.GLA), layers=_layers(P(mode=tl.GLA), 2, beta=A16)) == tl.TL_EINVAL
+    assert _commit_layers(P(mode=tl.GDN), layers=_layers(P(mode=tl.GDN), 2, beta=None)) == tl.TL_EINVAL
+    assert _commit_layers(P(batch=4, num_slots=3)) == tl.TL_EINVAL
+
+
+def test_accepted_path_checks():
+    for field in ("terminal", "path_len", "path"):
+        assert _accepted_path(P(), **{field: None}) == tl.TL_EINVAL
+        assert _accepted_path(P(), **{field: MIS}) == tl.TL_EINVAL
+    assert _accepted_path(P(batch=0), terminal=None, path_len=None, path=None) == tl.TL_OK

@@ -77,3 +77,29 @@ def test_pins_pass_unmutated():
     for check in PIN_CHECKS:
         check()
     assert oracle.step is _good_step
+
+
+def _path_leaf_first(parent_b, i):
+    out, j = [], int(i)
+    while j != -1:
+        out.append(j)
+        j = int(parent_b[j])
+    return out
+
+
+def _path_without_terminal(parent_b, i):
+    return _good_root_path(parent_b, i)[:-1]
+
+
+def _path_without_root(parent_b, i):
+    return _good_root_path(parent_b, i)[1:]
+
+
+_good_root_path = to.root_path
+
+
+@pytest.mark.parametrize("mut", [_path_leaf_first, _path_without_terminal, _path_without_root])
+def test_path_pins_reject_planted_mistakes(monkeypatch, mut):
+    monkeypatch.setattr(to, "root_path", mut)
+    with pytest.raises((AssertionError, oracle.OracleError)):
+        pins.test_accepted_paths_hand_derived()

@@ -420,3 +420,63 @@ def test_error_classes():
         oracle.check_problem(1, 3, 4, 128, 128, 64, GLA)
     with pytest.raises(oracle.Unsupported):
         oracle.check_problem(1, 1, 1, 128, 128, 257, GLA)
+
+
+# --------------------------------------------------------------------------
+# accepted path from a terminal node, and the cross-layer commit (§5.3)
+# --------------------------------------------------------------------------
+
+def test_accepted_paths_hand_derived():
+    """P(a) = Anc(a) u {a}, root first, on trees whose paths are known by hand:
+    a complete binary tree in BFS order (parent (i-1)//2), a chain, and a
+    two-root forest; -1 is the empty path."""
+    binary = np.array([-1] + [(i - 1) // 2 for i in range(1, 15)], np.int32)
+    chain = np.arange(-1, 9, dtype=np.int32)
+    forest = np.array([-1, 0, -1, 2, 3, 1, 3], np.int32)
+    parent = np.concatenate([binary, chain, forest, binary])
+    no = np.array([0, 15, 25, 32, 47], np.int32)
+    offs, path = oracle.accepted_paths(no, parent, [14, 6, 6, -1])
+    assert offs.tolist() == [0, 4, 11, 14, 14]
+    assert path.tolist() == [0, 2, 6, 14] + [0, 1, 2, 3, 4, 5, 6] + [2, 3, 6]
+    offs, path = oracle.accepted_paths(no, parent, [0, 9, 5, 7])
+    assert path.tolist() == [0] + list(range(10)) + [0, 1, 5] + [0, 1, 3, 7]
+    oracle.check_paths(no, parent, offs, path)
+
+
+def test_accepted_paths_errors():
+    no = np.array([0, 3], np.int32)
+    p = np.array([-1, 0, 0], np.int32)
+    for bad in (3, -2, 100):
+        with pytest.raises(oracle.BadPath):
+            oracle.accepted_paths(no, p, [bad])
+    with pytest.raises(oracle.BadTree):
+        oracle.accepted_paths(no, np.array([-1, 2, 0], np.int32), [1])
+    with pytest.raises(oracle.InvalidArg):
+        oracle.accepted_paths(no, p, [0, 1])
+
+
+@pytest.mark.parametrize("mode", [GLA, GDN])
+def test_commit_layers_is_each_layer_on_the_terminal_path(mode):
+    """Three layers with their own rows and states, the path of each request
+    written out by hand: every layer's result is the single-layer commit of
+    that hand path, and a request with terminal -1 keeps its state."""
+    rng = np.random.default_rng(16)
+    binary = np.array([-1] + [(i - 1) // 2 for i in range(1, 15)], np.int32)
+    parent = np.concatenate([binary, binary])
+    no = np.array([0, 15, 30], np.int32)
+    hand_offs = np.array([0, 4, 4], np.int32)
+    hand_path = np.array([0, 1, 4, 9], np.int32)        # terminal 9 in request 0, none in 1
+    layers = []
+    for _ in range(3):
+        k = rng.standard_normal((30, 2, 4))
+        k /= np.linalg.norm(k, axis=-1, keepdims=True)
+        v = rng.standard_normal((30, 4, 4))
+        g = -np.logaddexp(0.0, rng.standard_normal((30, 4)))
+        beta = 1.0 / (1.0 + np.exp(-rng.standard_normal((30, 4)))) if mode == GDN else None
+        layers.append((k, v, g, beta, rng.standard_normal((2, 4, 4, 4))))
+    got = oracle.commit_layers(mode, 2, no, parent, [9, -1], layers)
+    for (k, v, g, beta, st), new in zip(layers, got):
+        want = oracle.commit(mode, 2, no, parent, hand_offs, hand_path, k, v, g, beta, st)
+        np.testing.assert_array_equal(new, want)
+        np.testing.assert_array_equal(new[1], st[1])
+        assert not np.allclose(new[0], st[0])
