@@ -145,12 +145,25 @@ def gpu_leg(args, cfg, log):
         tl.commit(prob, u.node_offsets, u.parent, u.path_offsets, u.path, u.k, u.v, u.g, u.beta,
                   s.state, dev_err=err)
 
+    # the unified commit: every layer set in one call, each request's path
+    # given by its terminal node
+    terminal = torch.tensor([int(w.path[w.path_offsets[b + 1] - 1]) if w.path_offsets[b + 1] > w.path_offsets[b]
+                             else -1 for b in range(w.batch)], dtype=torch.int32, device="cuda:0")
+    table = [tl.layer(s.up.k, s.up.v, s.up.g, s.up.beta, s.state) for s in sets]
+
+    def run_commits():
+        if args.commit_layers:
+            tl.commit_layers(prob, table, sets[0].up.node_offsets, sets[0].up.parent, terminal,
+                             dev_err=err)
+        else:
+            for s in sets:
+                run_commit(s)
+
     rounds_w = max(1, math.ceil(args.warmup / R))
     for _ in range(rounds_w):
         for s in sets:
             run_verify(s)
-        for s in sets:
-            run_commit(s)
+        run_commits()
     torch.cuda.synchronize()
     if err.item() != 0:
         raise RuntimeError(f"device error {tl.status_string(err.item())}")
@@ -169,8 +182,7 @@ def gpu_leg(args, cfg, log):
         for s in sets:
             run_verify(s)
         ev[r][1].record(stream)
-        for s in sets:
-            run_commit(s)
+        run_commits()
         ev[r][2].record(stream)
     end.record(stream)
     torch.cuda.synchronize()
@@ -316,6 +328,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall time of the oracle sample (whole steps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--commit-layers", action="store_true",
+                    help="commit every layer set with one tree_state_commit_layers call")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only time a plain 512 MiB device copy (counter calibration)")
@@ -374,6 +388,8 @@ def main():
         },
         "verify_us": round(g["verify_ms"] * 1e3, 3),
         "commit_us": round(g["commit_ms"] * 1e3, 3),
+        "commit_call": "tree_state_commit_layers (all layer sets)" if args.commit_layers
+                       else "tree_state_commit (one per layer set)",
         "path_hbm_frac": round(path_frac, 4),
         "roofline": roofline,
         "cpu_baseline": cpu,
