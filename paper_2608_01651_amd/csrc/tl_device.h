@@ -268,6 +268,20 @@ __device__ inline void wait_vmem_below() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// LDS transpose read of 16-bit data (gfx950 ds_read_b64_tr_b16).  Within
+// each group of 16 lanes, lane s names 8 bytes (4 consecutive elements) at
+// `byte_off`; lane s receives element (s % 4) of the chunks named by lanes
+// s/4, s/4 + 4, s/4 + 8 and s/4 + 12 of its group, in that order.  So if
+// lane s names row r0 + s/4, columns c0 + 4 (s % 4) .. + 3 of a row-major
+// matrix, lane s gets column c0 + s of rows r0 .. r0 + 3: four consecutive
+// K values of an MFMA operand row, read from K-major storage.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+__device__ inline bf16x4 lds_read_tr16(const void* lds_base, uint32_t byte_off) {
+  typedef __attribute__((address_space(3))) s16x4* lp;
+  const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)lds_base + byte_off;
+  return __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lp)(uintptr_t)a));
+}
+
 // Output rows are written once and never read back by the kernel; NT
 // selects the non-temporal (streaming) cache policy for them.
 template <bool NT>

@@ -10,9 +10,11 @@
 //
 //  prologue  wave 0 loads the parents and gates and runs the topology (M+
 //            rows, cumulative log2-decay per head, per-tile OR of the M+ rows);
-//            waves 1..3 copy Q and K into LDS and stage V^T of every head.
-//            The state rows are requested after that, head by head, and
-//            arrive while the work that needs no state runs (the barriers
+//            waves 1..3 copy the Q, K and V rows of every head straight into
+//            swizzled row-major LDS (coalesced direct copies); V is read back
+//            as the K-major MFMA operand by LDS transpose reads.
+//            Every wave then requests head 0's state rows, which stream in
+//            while the work that needs no state runs (the barriers
 //            synchronise LDS only, so they do not wait for them).
 //  (a)       the lower-triangular 16x16 blocks (I, J), J <= I, of
 //            C_ij = [j in Anc(i) u {i}] 2^(cl_i - cl_j) (q_i . k_j) are spread
@@ -36,7 +38,7 @@
 namespace tl {
 
 struct GlaSmallLayout {
-  int cl, mask, tmask, flag, qst, kst, vt, total;
+  int cl, mask, tmask, flag, qst, kst, vst, total;
 };
 
 // LDS layout (bytes) of the <= 64-node path serving NH heads; identical on
@@ -56,7 +58,7 @@ __host__ __device__ inline GlaSmallLayout gla_small_layout(int D, int BV, int NH
     const int cb = NH * gla_small_slots(tm / kTile) * 2048;
     o += kb > cb ? kb : cb;
   }
-  L.vt = o;    o += NH * BV * gla_vt_stride(tm) * 2;    // V^T per head [BV][stride] bf16
+  L.vst = o;   o += NH * tm * BV * 2;                   // V rows per head, swizzled bf16
   L.total = o;
   return L;
 }
@@ -99,13 +101,11 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
   constexpr int MT = (MTILES + kWaves - 1) / kWaves;
   constexpr bool FULL = (MTILES % kWaves) == 0;   // every wave owns MT value tiles
   constexpr int CPRK = D / 8;
-  constexpr int VCH = BV / 8;                     // 16-byte chunks per value row
   constexpr int LT = kThreads - 64;               // loader threads (waves 1..3)
-  constexpr int VTN = (32 * VCH + LT - 1) / LT;   // V^T tasks per loader thread and head
+  static_assert(BV == D, "V rows are staged whole (one value slice per head)");
   constexpr int NTM = 4;                          // node tiles of a <= 64-node tree
   constexpr int NSLOT = gla_small_slots(NTM);     // C fragments per head
   constexpr int tm = 64;                          // the layout is always sized for 64 nodes
-  constexpr int TS = gla_vt_stride(tm);
   constexpr float kLog2e = 1.4426950408889634f;
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -118,7 +118,7 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
   int* s_flag = reinterpret_cast<int*>(tl_lds + L.flag);
   __bf16* s_q = reinterpret_cast<__bf16*>(tl_lds + L.qst);
   __bf16* s_k = reinterpret_cast<__bf16*>(tl_lds + L.kst);
-  __bf16* s_vt = reinterpret_cast<__bf16*>(tl_lds + L.vt);   // [NH][BV][TS]
+  __bf16* s_v = reinterpret_cast<__bf16*>(tl_lds + L.vst);   // [NH][tm][BV]
   unsigned char* s_cf = tl_lds + L.kst;   // C operand fragments, over the K rows after (a)
 
   const size_t qk_row = (size_t)a.Hk * D, v_row = (size_t)a.Hv * D;
@@ -130,24 +130,12 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
   auto mtile = [&](int m) { return wave * MT + m; };
   auto has_tile = [&](int m) { return FULL || mtile(m) < MTILES; };
 
-  // ---- prologue: loads, and the topology on wave 0
-  TL_TRACE_POINT(a, 1);
-  int par = -1;
-  float gx[NH];
-#pragma unroll
-  for (int hh = 0; hh < NH; ++hh) gx[hh] = 0.f;
-  if (wave == 0) {   // lanes >= T read node 0 (in bounds; ignored by the topology)
-    const int n = lane < T ? lane : 0;
-    par = a.parent[off + n];
-#pragma unroll
-    for (int hh = 0; hh < NH; ++hh) gx[hh] = a.g[(size_t)(off + n) * a.Hv + h0 + hh];
-  }
   // state rows of every head, in MFMA A-operand layout (rows = value channels).
-  // They are requested only once the tree, Q, K and V are in LDS, head by
-  // head, and waited for only by the head's state term: the memory system
-  // serves everything in flight together, so loads issued early would only
-  // slow down those needed first, and the work that needs no state (the
-  // coefficients C and the tree term) runs while the state streams in.
+  // Head 0's rows are requested right behind each wave's prologue loads and
+  // copies, so that HBM streams the state while the tree is staged; the
+  // prologue waits only for what was issued before them (vmcnt counts in
+  // issue order).  Later heads' rows follow once the coefficients C are
+  // formed, and each head's rows are waited for only by its state term.
   f32x4 sraw[NH][MT][KS][2];
   static_assert(FULL || MT == 1, "a wave owns all of its MT value tiles or none");
   auto load_state = [&](int hh) {
@@ -165,6 +153,27 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
     }
     issue_fence();
   };
+  // waits for every load and copy issued before load_state(0) (a wave that
+  // owns no value tile issued no state loads)
+  constexpr int NSL = (FULL ? MT : 1) * KS * 2;
+  auto wait_before_state = [&]() {
+    if (FULL || has_tile(0)) wait_vmem_below<NSL>();
+    else wait_vmem();
+  };
+  // ---- prologue: loads, and the topology on wave 0
+  TL_TRACE_POINT(a, 1);
+  int par = -1;
+  float gx[NH];
+#pragma unroll
+  for (int hh = 0; hh < NH; ++hh) gx[hh] = 0.f;
+  if (wave == 0) {   // lanes >= T read node 0 (in bounds; ignored by the topology)
+    const int n = lane < T ? lane : 0;
+    par = a.parent[off + n];
+#pragma unroll
+    for (int hh = 0; hh < NH; ++hh) gx[hh] = a.g[(size_t)(off + n) * a.Hv + h0 + hh];
+    load_state(0);
+    wait_before_state();
+  }
   if (wave == 0) {
     float cl[NH];
     uint64_t m1 = 0ull;
@@ -180,7 +189,6 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
     }
     if (lr == 0) s_tmask[lane / kTile] = tor;
   } else {
-    const int lt = tid - 64;
     // Q and K rows straight into swizzled LDS: one wave instruction moves
     // 64 / CPRK whole rows; lane l always fills chunk position l % CPRK
     {
@@ -199,50 +207,29 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
         }
       }
     }
-    // V rows -> registers -> V^T (two nodes per 32-bit word); task x is
-    // (8-column chunk x / 32, node pair x % 32), so consecutive lanes write
-    // consecutive V^T words.  The loads are unconditional (clamped to valid
-    // rows, the second node of a pair zeroed past T) so that the waits for
-    // them do not also wait for the state loads issued after them.
-    const int npair = (T + 1) >> 1;
-    bf16x8 v0[NH][VTN], v1[NH][VTN];
+    // V rows of every head the same way, for the rows of every 32-node
+    // chunk the tree term reads; rows past T repeat row T - 1 (finite values
+    // that meet zero coefficients)
+    {
+      constexpr int RPI = 64 / CPRK;
+      constexpr int RSTEP = LT / CPRK;
+      const int cpos = lane % CPRK;
+      const int TP = (T + 31) & ~31;
+      const uint32_t rbytes = (uint32_t)(v_row * 2);
 #pragma unroll
-    for (int hh = 0; hh < NH; ++hh) {
-      const __bf16* Vb = reinterpret_cast<const __bf16*>(a.v) + (size_t)off * v_row + (size_t)(h0 + hh) * D + slice * BV;
-#pragma unroll
-      for (int k = 0; k < VTN; ++k) {
-        const int x = lt + k * LT;
-        const int p = min(x & 31, npair - 1), cc = min(x >> 5, VCH - 1);
-        const int n1 = min(2 * p + 1, T - 1);
-        v0[hh][k] = *reinterpret_cast<const bf16x8*>(Vb + (uint32_t)(2 * p) * (uint32_t)v_row + cc * 8);
-        v1[hh][k] = *reinterpret_cast<const bf16x8*>(Vb + (uint32_t)n1 * (uint32_t)v_row + cc * 8);
-      }
-    }
-    // V^T columns 2*npair .. 32*ceil(T/32)-1 are read by the last chunk: zero
-    const int c0 = 2 * npair, c1 = (T + 31) & ~31;
-    const int nw = (c1 - c0) >> 1;   // < 16 words per row
-    if (nw > 0) {
-      for (int x = lt; x < NH * BV * 16; x += LT) {
-        const int v = x >> 4, w2 = x & 15;   // v runs over the rows of every head
-        if (w2 < nw) *reinterpret_cast<uint32_t*>(s_vt + v * TS + c0 + 2 * w2) = 0u;
-      }
-    }
-#pragma unroll
-    for (int hh = 0; hh < NH; ++hh) {
-#pragma unroll
-      for (int k = 0; k < VTN; ++k) {
-        const int x = lt + k * LT;
-        const int p = x & 31, cc = x >> 5;
-        if (cc < VCH && p < npair) {
-          const bool odd_in = 2 * p + 1 < T;
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            *reinterpret_cast<bf16x2*>(s_vt + (hh * BV + cc * 8 + e) * TS + 2 * p) =
-                bf16x2{v0[hh][k][e], odd_in ? v1[hh][k][e] : (__bf16)0.f};
+      for (int hh = 0; hh < NH; ++hh) {
+        const char* vb = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(a.v) + (size_t)off * v_row +
+                                                       (size_t)(h0 + hh) * D);
+        int r = (wave - 1) * RPI + lane / CPRK;
+        for (int base = (wave - 1) * 64; base < TP * CPRK; base += LT, r += RSTEP) {
+          const int rs = min(r, T - 1);
+          const uint32_t so = (uint32_t)rs * rbytes + (uint32_t)(swz<CPRK>(r, cpos) * 16);
+          copy16_to_lds_async(vb + so, s_v + (hh * tm * D) + base * 8);
         }
       }
     }
-    wait_vmem();   // the direct-to-LDS copies
+    load_state(0);
+    wait_before_state();   // the direct-to-LDS copies, not the state
   }
   TL_TRACE_POINT(a, 3);
   lds_barrier();   // Q, K, V^T, M+ rows, tile masks and cl are in LDS
@@ -251,7 +238,6 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
     return;
   }
   TL_TRACE_POINT(a, 4);
-  load_state(0);
 
   // operand fragment of row R + lr (R a multiple of 16), K chunk ks, from a
   // swizzled LDS matrix (fixed per-lane offsets inside a 16-row block)
@@ -341,14 +327,21 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
     }
   }
 
+  // transpose-read offsets: lane (lg, lr) names row 4 lg + lr / 4 of a
+  // 16-node half chunk and columns 16 mt + 4 (lr % 4) .. + 3, so it receives
+  // value channel 16 mt + lr of nodes 4 lg .. 4 lg + 3 (K positions kpos(lg, 0..3))
+  const int vrow_l = 4 * lg + (lr >> 2);
   int vo[MT];
 #pragma unroll
-  for (int m = 0; m < MT; ++m) vo[m] = ((kTile * mtile(m) + lr) * TS + 4 * lg) * 2;
+  for (int m = 0; m < MT; ++m) {
+    const int col = kTile * mtile(m) + 4 * (lr & 3);
+    vo[m] = vrow_l * D * 2 + swz<CPRK>(vrow_l, col >> 3) * 16 + (col & 7) * 2;
+  }
   f32x4 acc[NTM][MT];
 
   // tree term of head hh: acc = V^T (q_scale C)^T (needs no state)
   auto tree_term = [&](int hh) {
-    const unsigned char* vtbase = reinterpret_cast<const unsigned char*>(s_vt + hh * BV * TS);
+    const unsigned char* vbase = reinterpret_cast<const unsigned char*>(s_v + hh * tm * D);
 #pragma unroll
     for (int I = 0; I < NTM; ++I) {
 #pragma unroll
@@ -362,9 +355,10 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
 #pragma unroll
         for (int m = 0; m < MT; ++m) {
           if (has_tile(m)) {
-            const unsigned char* vrow = vtbase + vo[m] + 64 * c;
-            const bf16x4 x0 = *reinterpret_cast<const bf16x4*>(vrow);
-            const bf16x4 x1 = *reinterpret_cast<const bf16x4*>(vrow + 32);
+            // rows 32 c + vrow_l and 32 c + 16 + vrow_l keep the swizzle
+            // key of row vrow_l (32 c and 16 are multiples of CPRK)
+            const bf16x4 x0 = lds_read_tr16(vbase, vo[m] + (32 * c) * D * 2);
+            const bf16x4 x1 = lds_read_tr16(vbase, vo[m] + (32 * c + 16) * D * 2);
             const bf16x8 vf = bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
             acc[I][m] = mfma16(vf, chi, acc[I][m]);
             acc[I][m] = mfma16(vf, clo, acc[I][m]);
