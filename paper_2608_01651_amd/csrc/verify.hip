@@ -36,17 +36,15 @@
 //
 // Files: verify_gla_small.h (gated linear attention on MFMA, trees of <= 64
 // nodes), verify_tiled.hip (its own kernel: gated linear attention over
-// larger trees and the delta rule, node tile by node tile), verify_gla.h and
-// verify_gdn.h (the earlier per-wave MFMA paths, still used for shapes the
-// tiled kernel does not fit in LDS), verify_vector.h (vector path),
-// verify_common.h (layouts).
+// larger trees and the delta rule, node tile by node tile), verify_gdn.h (the
+// delta rule's per-wave MFMA path, for shapes whose tile-by-tile layout does
+// not fit in LDS), verify_vector.h (vector path), verify_common.h (layouts).
 #include <hip/hip_runtime.h>
 
 #include "tl_device.h"
 #include "tl_kernels.h"
 #include "verify_common.h"
 #include "verify_gdn.h"
-#include "verify_gla.h"
 #include "verify_gla_small.h"
 #include "verify_vector.h"
 
@@ -90,8 +88,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NH == 
   if constexpr (CAN_MFMA) {
     if (u.T >= kTile) {
       if constexpr (MODE == TL_MODE_GLA) {
-        if constexpr (W == 1) verify_gla_small<D, BV, NH>(a, u);
-        else verify_gla_mfma<D, BV, W>(a, u);
+        static_assert(W == 1, "larger trees of gated linear attention run in the tiled kernel");
+        verify_gla_small<D, BV, NH>(a, u);
       } else {
         verify_gdn_mfma<MODE, D, BV, W>(a, u);
       }
@@ -119,7 +117,7 @@ static tl_status launch_one(const VerifyArgs& a, hipStream_t stream) {
   VerifyLayout L = verify_layout(MODE, D, BV, F32IN ? 4 : 2, a.tm, W, false);
   if (CAN_MFMA) {
     int t;
-    if (MODE == TL_MODE_GLA) t = (W == 1) ? gla_small_layout(D, BV, NH).total : gla_layout(D, BV, a.tm, W).total;
+    if (MODE == TL_MODE_GLA) t = gla_small_layout(D, BV, NH).total;
     else t = verify_layout(MODE, D, BV, 2, a.tm, W, true).total;
     if (t > L.total) L.total = t;
   }
@@ -143,19 +141,24 @@ static tl_status launch_one(const VerifyArgs& a, hipStream_t stream) {
 // delta rule with d = 128 keeps U [tm][BV] in LDS, so 256-node trees use
 // 32-column value slices to stay within the 160 KB of LDS.  Gated linear
 // attention over trees of <= 64 nodes serves two grouped v-heads per block
-// when the group size is even.
+// when the group size is even (bf16 inputs, d >= 32).
 template <int MODE, int D, int BV, bool F32IN>
 static tl_status dispatch_w(const VerifyArgs& a, hipStream_t stream) {
-  if (F32IN) return launch_one<MODE, D, BV, F32IN, 4, 1>(a, stream);
-  if (a.tm > 128) {
-    if constexpr (MODE == TL_MODE_GDN && D == 128) return launch_one<MODE, D, 32, F32IN, 4, 1>(a, stream);
+  if constexpr (F32IN) {
     return launch_one<MODE, D, BV, F32IN, 4, 1>(a, stream);
-  }
-  if (a.tm > 64) return launch_one<MODE, D, BV, F32IN, 2, 1>(a, stream);
-  if constexpr (MODE == TL_MODE_GLA && D >= 32) {
+  } else if constexpr (MODE == TL_MODE_GLA && D >= 32) {
+    // trees of more than 64 nodes are served by the tiled kernel
+    if (a.tm > 64) return TL_EUNSUPPORTED;
     if ((a.Hv / a.Hk) % 2 == 0) return launch_one<MODE, D, BV, F32IN, 1, 2>(a, stream);
+    return launch_one<MODE, D, BV, F32IN, 1, 1>(a, stream);
+  } else {
+    if (a.tm > 128) {
+      if constexpr (MODE == TL_MODE_GDN && D == 128) return launch_one<MODE, D, 32, F32IN, 4, 1>(a, stream);
+      return launch_one<MODE, D, BV, F32IN, 4, 1>(a, stream);
+    }
+    if (a.tm > 64) return launch_one<MODE, D, BV, F32IN, 2, 1>(a, stream);
+    return launch_one<MODE, D, BV, F32IN, 1, 1>(a, stream);
   }
-  return launch_one<MODE, D, BV, F32IN, 1, 1>(a, stream);
 }
 
 template <int MODE, bool F32IN>

@@ -1,8 +1,8 @@
 // Verify, gated linear attention on MFMA, trees of 16..64 nodes.
 //
-// Same result as verify_gla_mfma (O^T = P .* (S Q^T) + V^T C^T per value
-// tile, Theorem 1 with U = V), organised so that the coefficient matrix C is
-// formed once per workgroup instead of once per wave, and so that a
+// Computes O^T = P .* (S Q^T) + V^T C^T per value tile (Theorem 1 with
+// U = V), organised so that the coefficient matrix C is formed once per
+// workgroup instead of once per wave, and so that a
 // workgroup can serve NH = 1 or 2 v-heads that share a qk-head (grouped
 // heads read the same q and k rows and the same tree, so K_J Q_I^T, the
 // M+ rows and the q/k traffic are shared; only the gates, the values and the
@@ -33,7 +33,6 @@
 #pragma once
 
 #include "verify_common.h"
-#include "verify_gla.h"
 
 namespace tl {
 

@@ -35,7 +35,6 @@
 #include "tl_device.h"
 #include "tl_kernels.h"
 #include "verify_common.h"
-#include "verify_gla.h"
 
 namespace tl {
 
