@@ -19,6 +19,7 @@ kernel must move, the roofline of the dominant kernel against the MI355X's
 from __future__ import annotations
 
 import argparse
+import re
 import hashlib
 import json
 import math
@@ -57,11 +58,15 @@ def commit_bytes(cfg, path_lens):
 
 
 def source_hash():
+    """Hash of the kernel sources' code: comments and whitespace are dropped,
+    so that only a change to what is compiled invalidates stored counters."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_01651_amd", "csrc")
     for f in sorted(os.listdir(csrc)):
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(f.encode() + fh.read())
+        with open(os.path.join(csrc, f), encoding="utf-8") as fh:
+            code = re.sub(r"/\*.*?\*/", " ", fh.read(), flags=re.S)
+        code = re.sub(r"//[^\n]*", " ", code)
+        h.update(f.encode() + " ".join(code.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -26,10 +26,12 @@
 //  3. readout: O^T = q_scale P_i (S Q_I^T) + U^T C^T (U = V for gated linear
 //     attention), stored as fp32.
 //
-// Two barriers per tile, before the chunk buffer is rewritten and after it
-// is written; they order LDS only, so the next tile's Q (and V) rows, loaded
-// a tile ahead, and the output stores stay in flight across them.  The state
-// is read once, split into bf16 hi + lo in registers.
+// When LDS holds two chunk buffers, the coefficients of tile I + 1 are
+// formed while tile I's value work runs, with one barrier per tile;
+// otherwise the two phases alternate, with two.  The barriers order LDS
+// only, so the Q (and V) rows, loaded two tiles ahead, and the output
+// stores of the previous tile stay in flight across them.  The state is read
+// once, split into bf16 hi + lo in registers.
 #include <hip/hip_runtime.h>
 
 #include "tl_device.h"
