@@ -9,3 +9,4 @@ from .tree_oracle import (  # noqa: F401
     check_problem, check_forest, check_paths, root_path, topology, step,
     verify, commit, prefix_state, accepted_paths, commit_layers,
 )
+from .conv_oracle import conv_gates, conv_state_commit  # noqa: F401,E402
