@@ -19,6 +19,7 @@ kernel must move, the roofline of the dominant kernel against the MI355X's
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import re
 import hashlib
 import json
@@ -55,6 +56,18 @@ def commit_bytes(cfg, path_lens):
     L = np.asarray(path_lens)
     per_row = Hk * dk * Q + Hv * dv * Q + Hv * 4 * (1 + gdn) + 4
     return int((L > 0).sum()) * 2 * Hv * dk * dv * 4 + int(L.sum()) * per_row + 4 * (L.size + 1)
+
+
+def conv_bytes(cfg, N, B, width):
+    """tree_conv_gates: every node's mixed row read once and q/k/v written
+    once (bf16), the gate inputs and outputs, the requests' state rows, the
+    layer's parameters and the forest.  A node's ancestor rows are the
+    ancestors' own rows: they are not counted again."""
+    gdn = 1 if cfg.mode == 1 else 0
+    Hk, Hv, dk, dv = cfg.num_qk_heads, cfg.num_v_heads, cfg.d_k, cfg.d_v
+    C = 2 * Hk * dk + Hv * dv
+    per_node = 2 * C * 2 + 2 * Hv * 4 * (1 + gdn) + 4
+    return N * per_node + B * (width - 1) * C * 2 + C * (width + 1) * 4 + 2 * Hv * 4 + 4 * (B + 1)
 
 
 def source_hash():
@@ -222,6 +235,75 @@ def gpu_leg(args, cfg, log):
                 verify_bytes=vb, commit_bytes=cb)
 
 
+def conv_leg(args, cfg, log):
+    """Times tree_conv_gates over resident layer sets (bf16 inputs)."""
+    import torch
+    from paper_2608_01651_amd import treelin as tl
+    from synth import workloads as W
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU (HIP) device")
+    tl.lib()
+    cfg = dataclasses.replace(cfg, in_dtype="bf16")
+    w = W.make(cfg, seed=args.seed)
+    ci = W.make_conv(w, width=args.conv_width)
+    Hk, Hv, dk, dv = cfg.num_qk_heads, cfg.num_v_heads, cfg.d_k, cfg.d_v
+    dev = "cuda:0"
+    cb = conv_bytes(cfg, w.N, w.batch, ci.width)
+    R = args.layers or max(1, math.ceil(2 * MALL_BYTES / cb))
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev).to(torch.bfloat16)
+    f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+    offs = torch.from_numpy(w.node_offsets.astype(np.int32)).to(dev)
+    par = torch.from_numpy(w.parent.astype(np.int32)).to(dev)
+    sets = []
+    for _ in range(R):
+        sets.append(dict(
+            x=bf(ci.x), ga=f32(ci.gate_a), gb=None if ci.gate_b is None else f32(ci.gate_b),
+            w=f32(ci.conv_weight), b=f32(ci.conv_bias), alog=f32(ci.A_log), dtb=f32(ci.dt_bias),
+            cs=bf(ci.conv_state),
+            q=torch.empty((w.N, Hk, dk), device=dev, dtype=torch.bfloat16),
+            k=torch.empty((w.N, Hk, dk), device=dev, dtype=torch.bfloat16),
+            v=torch.empty((w.N, Hv, dv), device=dev, dtype=torch.bfloat16),
+            g=torch.empty((w.N, Hv), device=dev),
+            beta=torch.empty((w.N, Hv), device=dev) if cfg.mode == W.GDN else None))
+    log(f"conv front end: {cfg.name} B={w.batch} N={w.N} C={2 * Hk * dk + Hv * dv} width={ci.width}, "
+        f"{R} layer sets ({R * cb / 1e6:.0f} MB)")
+    prob = tl.problem(w.batch, Hk, Hv, dk, dv, cfg.max_nodes, mode=cfg.mode, in_dtype=tl.BF16)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def run(s):
+        tl.conv_gates(prob, ci.width, offs, par, s["x"], s["ga"], s["gb"], s["w"], s["b"], s["alog"],
+                      s["dtb"], s["cs"], s["q"], s["k"], s["v"], s["g"], s["beta"], dev_err=err)
+
+    for _ in range(max(1, math.ceil(args.warmup / R))):
+        for s in sets:
+            run(s)
+    torch.cuda.synchronize()
+    rounds = max(1, math.ceil(args.steps / R))
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(rounds):
+        for s in sets:
+            run(s)
+    end.record()
+    torch.cuda.synchronize()
+    if err.item() != 0:
+        raise RuntimeError(f"device error {tl.status_string(err.item())}")
+    us = start.elapsed_time(end) * 1e3 / (rounds * R)
+    achieved = cb / (us * 1e-6) / 1e9
+    return {
+        "metric": "tree-parallel convolution front end: tree nodes/s per layer; % of HBM roofline (1 MI355X)",
+        "value": round(w.N / (us * 1e-6), 1), "unit": "tree-tokens/s", "n_gpus": 1,
+        "steps": rounds * R, "warmup": args.warmup, "us_per_launch": round(us, 3),
+        "higher_is_better": True, "dtype": "bf16 in/out, f32 arithmetic", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: B={w.batch}, {w.N} tree nodes, Hk={Hk}, Hv={Hv}, "
+                               f"d_k=d_v={dk}, conv width {ci.width}", "layer_sets": R},
+        "roofline": {"bound": "hbm", "kernel": "tree_conv_gates", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "algorithmic_bytes_per_launch": int(cb)},
+    }
+
+
 # ---------------------------------------------------------------------------
 # CPU baseline: the fp64 oracle on a bounded sample of the same workload
 # ---------------------------------------------------------------------------
@@ -352,6 +434,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall time of the oracle sample (whole steps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--conv", action="store_true",
+                    help="time the tree-parallel convolution front end (tree_conv_gates) instead")
+    ap.add_argument("--conv-width", type=int, default=4)
     ap.add_argument("--commit-layers", action="store_true",
                     help="commit every layer set with one tree_state_commit_layers call")
     ap.add_argument("--quiet", action="store_true")
@@ -373,6 +458,9 @@ def main():
         return
     from synth import workloads as W
     cfg = W.CONFIGS[args.workload]
+    if args.conv:
+        print(json.dumps(conv_leg(args, cfg, log)), flush=True)
+        return
     cpu = None
     if not args.no_cpu_baseline:
         # before the GPU is touched, so the worker pool may fork

@@ -182,6 +182,52 @@ tl_status tree_accepted_path(const tl_problem* problem,
                              int32_t* path,           /* [N] */
                              int32_t* dev_err, void* stream);
 
+/* Tree-parallel convolution front end (§4.3 "Stage 1: tree-parallel
+ * convolution and gate preparation"; the convolution and gates of §2.1).
+ *
+ * For every node i, with C = 2 Hk d_k + Hv d_v channels and w = conv_width
+ * (2..4):
+ *   y_i[c] = conv_bias[c] + sum_{p<w} conv_weight[c, p] * s_i[p][c]
+ * where s_i is the last w rows of (the request's convolution state rows,
+ * then the x rows of the node's root path, root first): p = w-1 is node i,
+ * p = w-2 its parent, and above the root the window continues into the
+ * committed state.  z = y * sigmoid(y) (SiLU) is split into q | k | v; q
+ * and k are normalised per head, z / sqrt(sum z^2 + norm_eps), and all three
+ * are stored as bf16 (round to nearest even).  Gates per (node, v-head):
+ *   g = -exp(A_log[h]) * softplus(gate_a + dt_bias[h])   (the log-decay
+ *       tree_lin_attn_verify takes),
+ *   beta = sigmoid(gate_b)                               (delta rule only).
+ * The arithmetic is fp32.
+ * Layouts: x [N, C] bf16 (channels q | k | v, head-major); gate_a, gate_b
+ *   [N, Hv] fp32; conv_weight [C, w] fp32; conv_bias [C] fp32; A_log,
+ *   dt_bias [Hv] fp32; conv_state [num_slots, w-1, C] bf16, rows oldest
+ *   first; outputs q, k [N, Hk, d_k], v [N, Hv, d_v] bf16, g, beta [N, Hv]
+ *   fp32.  problem->in_dtype must be TL_BF16.  gate_b and beta are NULL for
+ *   TL_MODE_GLA and non-NULL for TL_MODE_GDN.  x, conv_state, q, k, v,
+ *   conv_weight and conv_bias must be 16-byte aligned.
+ * Device errors: TL_EBADTREE (forest), TL_EINVAL (slot index); that
+ * request's rows are left unwritten. */
+tl_status tree_conv_gates(const tl_problem* problem, int32_t conv_width, float norm_eps,
+                          const int32_t* node_offsets, const int32_t* parent,
+                          const void* x, const float* gate_a, const float* gate_b,
+                          const float* conv_weight, const float* conv_bias,
+                          const float* A_log, const float* dt_bias,
+                          const void* conv_state, const int32_t* slot,
+                          void* q, void* k, void* v, float* g, float* beta,
+                          int32_t* dev_err, void* stream);
+
+/* Convolution-state commit: the state of request b becomes the last w-1 rows
+ * of (its state rows, the x rows of the accepted path ending at terminal[b],
+ * root first), written in place; terminal -1 leaves it untouched.  Enqueue
+ * after the tree_conv_gates call that reads the same slots.  The rows are
+ * copied exactly (bf16).  Device errors: TL_EBADTREE, TL_EBADPATH (terminal
+ * outside [-1, T_b)), TL_EINVAL (slot index); that slot is left untouched. */
+tl_status tree_conv_state_commit(const tl_problem* problem, int32_t conv_width,
+                                 const int32_t* node_offsets, const int32_t* parent,
+                                 const int32_t* terminal, const void* x,
+                                 void* conv_state, const int32_t* slot,
+                                 int32_t* dev_err, void* stream);
+
 /* Tree topology of §4.1's notation table, as the kernels build it:
  * anc_mask[r, w] (W = ceil(max_nodes/64) uint64 words per node) has bit
  * (j mod 64) of word j/64 set iff local node j is r's node itself or one of

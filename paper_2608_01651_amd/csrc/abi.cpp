@@ -197,6 +197,91 @@ tl_status tree_topology_export(const tl_problem* problem, const int32_t* node_of
   return tl::launch_topology(a, reinterpret_cast<hipStream_t>(stream));
 }
 
+tl_status tree_conv_gates(const tl_problem* problem, int32_t conv_width, float norm_eps,
+                          const int32_t* node_offsets, const int32_t* parent, const void* x,
+                          const float* gate_a, const float* gate_b, const float* conv_weight,
+                          const float* conv_bias, const float* A_log, const float* dt_bias,
+                          const void* conv_state, const int32_t* slot, void* q, void* k, void* v,
+                          float* g, float* beta, int32_t* dev_err, void* stream) {
+  tl_status st = check_problem(problem);
+  if (st != TL_OK) return st;
+  if (conv_width < 2 || conv_width > 4 || problem->in_dtype != TL_BF16) return TL_EUNSUPPORTED;
+  if (!(norm_eps >= 0.f)) return TL_EINVAL;
+  if (problem->batch == 0) return TL_OK;
+  const bool gdn = problem->mode == TL_MODE_GDN;
+  if (!node_offsets || !parent || !x || !gate_a || !conv_weight || !conv_bias || !A_log ||
+      !dt_bias || !conv_state || !q || !k || !v || !g)
+    return TL_EINVAL;
+  if (gdn != (gate_b != nullptr) || gdn != (beta != nullptr)) return TL_EINVAL;
+  if (!aligned(x, 16) || !aligned(conv_state, 16) || !aligned(q, 16) || !aligned(k, 16) ||
+      !aligned(v, 16) || !aligned(conv_weight, 16) || !aligned(conv_bias, 16))
+    return TL_EINVAL;
+  if (!aligned(node_offsets, 4) || !aligned(parent, 4) || !aligned(gate_a, 4) || !aligned(A_log, 4) ||
+      !aligned(dt_bias, 4) || !aligned(g, 4) || (gate_b && !aligned(gate_b, 4)) ||
+      (beta && !aligned(beta, 4)) || (slot && !aligned(slot, 4)) || (dev_err && !aligned(dev_err, 4)))
+    return TL_EINVAL;
+  if (!slot && problem->num_slots < problem->batch) return TL_EINVAL;
+  tl::ConvArgs a;
+  a.node_offsets = node_offsets;
+  a.parent = parent;
+  a.x = x;
+  a.gate_a = gate_a;
+  a.gate_b = gate_b;
+  a.conv_weight = conv_weight;
+  a.conv_bias = conv_bias;
+  a.A_log = A_log;
+  a.dt_bias = dt_bias;
+  a.conv_state = conv_state;
+  a.slot = slot;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.g = g;
+  a.beta = beta;
+  a.dev_err = dev_err;
+  a.batch = problem->batch;
+  a.Hk = problem->num_qk_heads;
+  a.Hv = problem->num_v_heads;
+  a.dk = problem->d_k;
+  a.dv = problem->d_v;
+  a.C = 2 * a.Hk * a.dk + a.Hv * a.dv;
+  a.max_nodes = problem->max_nodes;
+  a.num_slots = problem->num_slots;
+  a.tiles = 0;
+  a.eps = norm_eps;
+  return tl::launch_conv_gates(a, conv_width, gdn, reinterpret_cast<hipStream_t>(stream));
+}
+
+tl_status tree_conv_state_commit(const tl_problem* problem, int32_t conv_width,
+                                 const int32_t* node_offsets, const int32_t* parent,
+                                 const int32_t* terminal, const void* x, void* conv_state,
+                                 const int32_t* slot, int32_t* dev_err, void* stream) {
+  tl_status st = check_problem(problem);
+  if (st != TL_OK) return st;
+  if (conv_width < 2 || conv_width > 4 || problem->in_dtype != TL_BF16) return TL_EUNSUPPORTED;
+  if (problem->batch == 0) return TL_OK;
+  if (!node_offsets || !parent || !terminal || !x || !conv_state) return TL_EINVAL;
+  if (!aligned(x, 16) || !aligned(conv_state, 16) || !aligned(node_offsets, 4) ||
+      !aligned(parent, 4) || !aligned(terminal, 4) || (slot && !aligned(slot, 4)) ||
+      (dev_err && !aligned(dev_err, 4)))
+    return TL_EINVAL;
+  if (!slot && problem->num_slots < problem->batch) return TL_EINVAL;
+  tl::ConvCommitArgs a;
+  a.node_offsets = node_offsets;
+  a.parent = parent;
+  a.terminal = terminal;
+  a.x = x;
+  a.conv_state = conv_state;
+  a.slot = slot;
+  a.dev_err = dev_err;
+  a.batch = problem->batch;
+  a.C = 2 * problem->num_qk_heads * problem->d_k + problem->num_v_heads * problem->d_v;
+  a.max_nodes = problem->max_nodes;
+  a.num_slots = problem->num_slots;
+  a.tiles = (a.C + tl::kConvCommitTile - 1) / tl::kConvCommitTile;
+  return tl::launch_conv_state_commit(a, conv_width, reinterpret_cast<hipStream_t>(stream));
+}
+
 const char* tl_status_string(tl_status s) {
   switch (s) {
     case TL_OK: return "TL_OK: success";

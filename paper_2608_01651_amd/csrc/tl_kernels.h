@@ -91,6 +91,46 @@ struct TopoArgs {
   int batch, max_nodes, words;
 };
 
+// Channels per workgroup of the convolution-state commit (256 threads x 8);
+// conv_gates picks its own channel tile by tree size.
+constexpr int kConvCommitTile = 2048;
+
+// tree_conv_gates
+struct ConvArgs {
+  const int32_t* node_offsets;
+  const int32_t* parent;
+  const void* x;
+  const float* gate_a;
+  const float* gate_b;
+  const float* conv_weight;
+  const float* conv_bias;
+  const float* A_log;
+  const float* dt_bias;
+  const void* conv_state;
+  const int32_t* slot;
+  void* q;
+  void* k;
+  void* v;
+  float* g;
+  float* beta;
+  int32_t* dev_err;
+  int batch, Hk, Hv, dk, dv, C, max_nodes, num_slots;
+  int tiles;   // channel tiles per request (set by the launcher)
+  float eps;
+};
+
+// tree_conv_state_commit
+struct ConvCommitArgs {
+  const int32_t* node_offsets;
+  const int32_t* parent;
+  const int32_t* terminal;
+  const void* x;
+  void* conv_state;
+  const int32_t* slot;
+  int32_t* dev_err;
+  int batch, C, max_nodes, num_slots, tiles;
+};
+
 tl_status launch_verify(const tl_problem& p, const VerifyArgs& a, hipStream_t stream);
 tl_status launch_verify_tiled(const tl_problem& p, const VerifyArgs& a, hipStream_t stream);
 int verify_tiled_lds_bytes(int mode, int d, int tm, int W);
@@ -98,6 +138,8 @@ tl_status launch_commit(const tl_problem& p, const CommitArgs& a, hipStream_t st
 tl_status launch_commit_layers(const tl_problem& p, const CommitLayersArgs& a, hipStream_t stream);
 tl_status launch_accepted_path(const PathArgs& a, hipStream_t stream);
 tl_status launch_topology(const TopoArgs& a, hipStream_t stream);
+tl_status launch_conv_gates(const ConvArgs& a, int width, bool gdn, hipStream_t stream);
+tl_status launch_conv_state_commit(const ConvCommitArgs& a, int width, hipStream_t stream);
 int verify_lds_bytes(const tl_problem& p, int tm);
 
 }  // namespace tl

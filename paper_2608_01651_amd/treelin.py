@@ -78,6 +78,10 @@ def lib():
         L.tree_state_commit_layers.restype = ctypes.c_int
         L.tree_accepted_path.argtypes = [P] + [vp] * 7
         L.tree_accepted_path.restype = ctypes.c_int
+        L.tree_conv_gates.argtypes = [P, ctypes.c_int32, ctypes.c_float] + [vp] * 18
+        L.tree_conv_gates.restype = ctypes.c_int
+        L.tree_conv_state_commit.argtypes = [P, ctypes.c_int32] + [vp] * 8
+        L.tree_conv_state_commit.restype = ctypes.c_int
         L.tree_topology_export.argtypes = [P] + [vp] * 6
         L.tree_topology_export.restype = ctypes.c_int
         L.tl_status_string.argtypes = [ctypes.c_int]
@@ -194,3 +198,33 @@ def accepted_path(prob, node_offsets, parent, terminal, path_len, path, dev_err=
         _ptr(terminal, "terminal", _I32), _ptr(path_len, "path_len", _I32), _ptr(path, "path", _I32),
         _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
     _check(s, "tree_accepted_path")
+
+
+_BF = (torch.bfloat16,)
+
+
+def conv_gates(prob, width, node_offsets, parent, x, gate_a, gate_b, conv_weight, conv_bias,
+               A_log, dt_bias, conv_state, q, k, v, g, beta, slot=None, eps=1e-6, dev_err=None,
+               stream=None):
+    """tree_conv_gates: q, k, v (bf16) and g, beta (fp32) of every node from its
+    mixed projection row x and its root-path convolution window."""
+    s = lib().tree_conv_gates(
+        ctypes.byref(prob), int(width), float(eps), _ptr(node_offsets, "node_offsets", _I32),
+        _ptr(parent, "parent", _I32), _ptr(x, "x", _BF), _ptr(gate_a, "gate_a", _F32),
+        _ptr(gate_b, "gate_b", _F32, True), _ptr(conv_weight, "conv_weight", _F32),
+        _ptr(conv_bias, "conv_bias", _F32), _ptr(A_log, "A_log", _F32), _ptr(dt_bias, "dt_bias", _F32),
+        _ptr(conv_state, "conv_state", _BF), _ptr(slot, "slot", _I32, True), _ptr(q, "q", _BF),
+        _ptr(k, "k", _BF), _ptr(v, "v", _BF), _ptr(g, "g", _F32), _ptr(beta, "beta", _F32, True),
+        _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
+    _check(s, "tree_conv_gates")
+
+
+def conv_state_commit(prob, width, node_offsets, parent, terminal, x, conv_state, slot=None,
+                      dev_err=None, stream=None):
+    """tree_conv_state_commit: shifts the accepted path's x rows into the convolution state."""
+    s = lib().tree_conv_state_commit(
+        ctypes.byref(prob), int(width), _ptr(node_offsets, "node_offsets", _I32),
+        _ptr(parent, "parent", _I32), _ptr(terminal, "terminal", _I32), _ptr(x, "x", _BF),
+        _ptr(conv_state, "conv_state", _BF), _ptr(slot, "slot", _I32, True),
+        _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
+    _check(s, "tree_conv_state_commit")

@@ -353,3 +353,58 @@ def prefix_chunks(cfg):
     if isinstance(cfg, str):
         cfg = CONFIGS[cfg]
     return math.ceil(cfg.prefix_len / PREFIX_CHUNK)
+
+
+# --------------------------------------------------------------------------
+# inputs of the convolution front end (drawn values only)
+# --------------------------------------------------------------------------
+_S_CONV_X, _S_CONV_GA, _S_CONV_GB, _S_CONV_STATE = range(20, 24)
+_S_CONV_PARAMS = 30
+
+
+@dataclasses.dataclass
+class ConvInputs:
+    width: int
+    x: np.ndarray                  # [N, C] float32, bf16-representable; C = 2 Hk d_k + Hv d_v
+    gate_a: np.ndarray             # [N, Hv] float32 (decay gate pre-activation)
+    gate_b: np.ndarray | None      # [N, Hv] float32 (write gate pre-activation; delta rule)
+    conv_weight: np.ndarray        # [C, width] float32
+    conv_bias: np.ndarray          # [C] float32
+    A_log: np.ndarray              # [Hv] float32
+    dt_bias: np.ndarray            # [Hv] float32
+    conv_state: np.ndarray         # [B, width - 1, C] float32, bf16-representable
+
+
+def make_conv(w, width=4, requests=None):
+    """Front-end inputs over the forest of workload w: per request (seeded by
+    request id, like the tree tokens) the mixed projection rows x ~ N(0,1),
+    the gate pre-activations ~ N(0,1) and the committed convolution state
+    rows ~ N(0,1); per layer the convolution weights ~ N(0, 1/width), bias
+    ~ N(0, 0.1^2), A_log = log U(1, 16) and dt_bias = inverse softplus of
+    dt = exp U(log 1e-3, log 1e-1) (the usual Gated DeltaNet initialisation)."""
+    cfg = w.cfg
+    Hk, Hv, dk, dv = cfg.num_qk_heads, cfg.num_v_heads, cfg.d_k, cfg.d_v
+    C = 2 * Hk * dk + Hv * dv
+    requests = list(range(w.batch)) if requests is None else list(requests)
+    assert len(requests) == w.batch
+    xs, gas, gbs, sts = [], [], [], []
+    for i, b in enumerate(requests):
+        T = int(w.node_offsets[i + 1] - w.node_offsets[i])
+        xs.append(_rng(w.seed, cfg, w.step, b, _S_CONV_X).standard_normal((T, C)))
+        gas.append(_rng(w.seed, cfg, w.step, b, _S_CONV_GA).standard_normal((T, Hv)))
+        gbs.append(_rng(w.seed, cfg, w.step, b, _S_CONV_GB).standard_normal((T, Hv)))
+        sts.append(_rng(w.seed, cfg, w.step, b, _S_CONV_STATE).standard_normal((width - 1, C)))
+    prm = _rng(w.seed, cfg, 0, 0, _S_CONV_PARAMS)
+    dt = np.exp(prm.uniform(math.log(1e-3), math.log(1e-1), Hv))
+    f32 = lambda a: np.asarray(a, dtype=np.float32)
+    cat = lambda parts, cols: np.concatenate(parts) if parts else np.zeros((0, cols))
+    return ConvInputs(
+        width=width,
+        x=round_bf16(f32(cat(xs, C))),
+        gate_a=f32(cat(gas, Hv)),
+        gate_b=f32(cat(gbs, Hv)) if cfg.mode == GDN else None,
+        conv_weight=f32(prm.standard_normal((C, width)) / math.sqrt(width)),
+        conv_bias=f32(0.1 * prm.standard_normal(C)),
+        A_log=f32(np.log(prm.uniform(1.0, 16.0, Hv))),
+        dt_bias=f32(dt + np.log(-np.expm1(-dt))),
+        conv_state=round_bf16(f32(np.stack(sts))) if sts else np.zeros((0, width - 1, C), np.float32))

@@ -33,7 +33,8 @@ def test_library_exports_every_declared_function():
     L = _lib_or_build()
     names = _declared_functions()
     assert {"tree_lin_attn_verify", "tree_state_commit", "tree_topology_export",
-            "tree_state_commit_layers", "tree_accepted_path",
+            "tree_state_commit_layers", "tree_accepted_path", "tree_conv_gates",
+            "tree_conv_state_commit",
             "tl_status_string", "tl_version"} <= set(names)
     for n in names:
         assert hasattr(L, n), f"{n} declared in include/treelin.h but not exported"
@@ -192,3 +193,46 @@ def test_accepted_path_checks():
         assert _accepted_path(P(), **{field: None}) == tl.TL_EINVAL
         assert _accepted_path(P(), **{field: MIS}) == tl.TL_EINVAL
     assert _accepted_path(P(batch=0), terminal=None, path_len=None, path=None) == tl.TL_OK
+
+
+def _conv(prob, width=4, eps=1e-6, **kw):
+    gdn = prob is not None and prob.mode == tl.GDN
+    f = dict(offs=A16, par=A16, x=A16, ga=A16, gb=A16 if gdn else None, w=A16, bias=A16, alog=A16,
+             dtb=A16, cs=A16, slot=None, q=A16, k=A16, v=A16, g=A16, beta=A16 if gdn else None)
+    f.update(kw)
+    return _lib_or_build().tree_conv_gates(
+        None if prob is None else ctypes.byref(prob), width, eps, f["offs"], f["par"], f["x"], f["ga"],
+        f["gb"], f["w"], f["bias"], f["alog"], f["dtb"], f["cs"], f["slot"], f["q"], f["k"], f["v"],
+        f["g"], f["beta"], None, None)
+
+
+def _conv_commit(prob, width=4, **kw):
+    f = dict(offs=A16, par=A16, term=A16, x=A16, cs=A16)
+    f.update(kw)
+    return _lib_or_build().tree_conv_state_commit(
+        None if prob is None else ctypes.byref(prob), width, f["offs"], f["par"], f["term"], f["x"],
+        f["cs"], None, None, None)
+
+
+def test_conv_entry_points_checks():
+    for mode in (tl.GLA, tl.GDN):
+        assert _conv(P(mode=mode, batch=0)) == tl.TL_OK
+    for width in (1, 5):
+        assert _conv(P(), width=width) == tl.TL_EUNSUPPORTED
+        assert _conv_commit(P(), width=width) == tl.TL_EUNSUPPORTED
+    assert _conv(P(in_dtype=tl.F32)) == tl.TL_EUNSUPPORTED
+    assert _conv_commit(P(in_dtype=tl.F32)) == tl.TL_EUNSUPPORTED
+    assert _conv(P(), eps=-1.0) == tl.TL_EINVAL
+    assert _conv(P(mode=tl.GLA), gb=A16) == tl.TL_EINVAL
+    assert _conv(P(mode=tl.GLA), beta=A16) == tl.TL_EINVAL
+    assert _conv(P(mode=tl.GDN), gb=None) == tl.TL_EINVAL
+    assert _conv(P(mode=tl.GDN), beta=None) == tl.TL_EINVAL
+    for field in ("offs", "par", "x", "ga", "w", "bias", "alog", "dtb", "cs", "q", "k", "v", "g"):
+        assert _conv(P(), **{field: None}) == tl.TL_EINVAL, field
+    for field in ("x", "cs", "q", "k", "v", "w", "bias"):
+        assert _conv(P(), **{field: A16 + 4}) == tl.TL_EINVAL, field
+    assert _conv(P(batch=4, num_slots=3)) == tl.TL_EINVAL
+    for field in ("offs", "par", "term", "x", "cs"):
+        assert _conv_commit(P(), **{field: None}) == tl.TL_EINVAL, field
+    assert _conv_commit(P(), x=A16 + 4) == tl.TL_EINVAL
+    assert _conv_commit(P(batch=0), offs=None) == tl.TL_OK
