@@ -141,8 +141,11 @@ def gpu_leg(args, cfg, log):
         state0 = torch.from_numpy(w.state).to("cuda:0")
     vb = verify_bytes(cfg, w.N, w.batch)
     cb = commit_bytes(cfg, np.diff(w.path_offsets))
-    # a layer set's footprint is what verify touches: state, q/k/v/gates, output
-    R = args.layers or max(1, math.ceil(2 * MALL_BYTES / vb))
+    # a layer set's footprint is what verify touches: state, q/k/v/gates,
+    # output; enough sets to exceed the Infinity Cache twice, at most 64 (the
+    # latency-bound shapes have footprints of kilobytes, and a captured round
+    # holds two launches per set)
+    R = args.layers or min(64, max(1, math.ceil(2 * MALL_BYTES / vb)))
     sets = []
     for r in range(R):
         sets.append(LayerSet(w, state0.clone(), torch))
@@ -189,6 +192,30 @@ def gpu_leg(args, cfg, log):
     rounds = max(1, math.ceil(args.steps / R))
     steps = rounds * R
 
+    def one_round():
+        for s in sets:
+            run_verify(s)
+        run_commits()
+
+    graph = None
+    if args.graph:
+        # one round (R verifies, then the commits) captured once and replayed;
+        # the kernels read every size from device memory, so replays need no
+        # host work
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            one_round()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            one_round()
+        torch.cuda.synchronize()
+        for _ in range(rounds_w):
+            graph.replay()
+        torch.cuda.synchronize()
+
     def timed_steps():
         # the headline pass: only a start and an end event around the steps
         # (markers between kernels would perturb what they measure)
@@ -197,9 +224,10 @@ def gpu_leg(args, cfg, log):
         torch.cuda.synchronize()
         start.record(stream)
         for _ in range(rounds):
-            for s in sets:
-                run_verify(s)
-            run_commits()
+            if graph is not None:
+                graph.replay()
+            else:
+                one_round()
         end.record(stream)
         torch.cuda.synchronize()
         return start.elapsed_time(end)
@@ -250,7 +278,7 @@ def conv_leg(args, cfg, log):
     Hk, Hv, dk, dv = cfg.num_qk_heads, cfg.num_v_heads, cfg.d_k, cfg.d_v
     dev = "cuda:0"
     cb = conv_bytes(cfg, w.N, w.batch, ci.width)
-    R = args.layers or max(1, math.ceil(2 * MALL_BYTES / cb))
+    R = args.layers or min(64, max(1, math.ceil(2 * MALL_BYTES / cb)))
     bf = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev).to(torch.bfloat16)
     f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
     offs = torch.from_numpy(w.node_offsets.astype(np.int32)).to(dev)
@@ -437,6 +465,8 @@ def main():
     ap.add_argument("--conv", action="store_true",
                     help="time the tree-parallel convolution front end (tree_conv_gates) instead")
     ap.add_argument("--conv-width", type=int, default=4)
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one round of launches in a HIP graph and time its replays")
     ap.add_argument("--commit-layers", action="store_true",
                     help="commit every layer set with one tree_state_commit_layers call")
     ap.add_argument("--quiet", action="store_true")
@@ -498,8 +528,10 @@ def main():
             "batch": w.batch, "tree_nodes": w.N, "accepted_rows": int(w.path.size),
             "in_dtype": cfg.in_dtype, "layer_sets": g["R"], "parallelism": "none (1 GPU)",
         },
-        "timing": "value and ms_per_step from one pass with an event before and after the timed steps; "
-                  "verify_us and commit_us from a second pass with events around each round's launches",
+        "timing": ("value and ms_per_step from replays of a captured HIP graph of one round; "
+                   if args.graph else
+                   "value and ms_per_step from one pass with an event before and after the timed steps; ")
+                  + "verify_us and commit_us from a second, eager pass with events around each round's launches",
         "verify_us": round(g["verify_ms"] * 1e3, 3),
         "commit_us": round(g["commit_ms"] * 1e3, 3),
         "commit_call": "tree_state_commit_layers (all layer sets)" if args.commit_layers
