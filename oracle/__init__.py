@@ -10,3 +10,4 @@ from .tree_oracle import (  # noqa: F401
     verify, commit, prefix_state, accepted_paths, commit_layers,
 )
 from .conv_oracle import conv_gates, conv_state_commit  # noqa: F401,E402
+from .budget_oracle import budget_select, path_scores  # noqa: F401,E402

@@ -408,3 +408,52 @@ def make_conv(w, width=4, requests=None):
         A_log=f32(np.log(prm.uniform(1.0, 16.0, Hv))),
         dt_bias=f32(dt + np.log(-np.expm1(-dt))),
         conv_state=round_bf16(f32(np.stack(sts))) if sts else np.zeros((0, width - 1, C), np.float32))
+
+
+# --------------------------------------------------------------------------
+# candidate trees with draft probabilities (inputs of the budget allocation)
+# --------------------------------------------------------------------------
+_S_CAND = 50
+
+
+def candidate_tree(rng, branching, depth_cap, quantum=None):
+    """A drafter's candidate tree in BFS order: depth-l nodes get branching[l]
+    children (1 past the end of the list) down to depth_cap; each sibling
+    group's draft probabilities are softmax(N(0,1)), rounded to multiples of
+    `quantum` (at least one quantum) when given, so that equal path scores
+    occur.  The root's probability is 1.  Returns (parent int32, prob
+    float32)."""
+    parent, prob, frontier = [-1], [1.0], [0]
+    for lvl in range(depth_cap):
+        nb = branching[lvl] if lvl < len(branching) else 1
+        nxt = []
+        for p in frontier:
+            z = rng.standard_normal(nb)
+            pr = np.exp(z - z.max())
+            pr /= pr.sum()
+            if quantum:
+                pr = np.maximum(np.round(pr / quantum), 1.0) * quantum
+            for c in range(nb):
+                parent.append(p)
+                prob.append(float(pr[c]))
+                nxt.append(len(parent) - 1)
+        frontier = nxt
+    return np.asarray(parent, np.int32), np.asarray(prob, np.float32)
+
+
+def make_candidates(seed, sizes, quantum=None):
+    """A batch of candidate trees: sizes[b] = (branching, depth_cap), or None
+    for a request with no candidates.  Returns cand_offsets [B+1], parent [M],
+    prob [M]."""
+    parents, probs = [], []
+    for b, spec in enumerate(sizes):
+        if spec is None:
+            parents.append(np.zeros(0, np.int32))
+            probs.append(np.zeros(0, np.float32))
+            continue
+        rng = np.random.default_rng([seed, 0, 0, b, _S_CAND])
+        p, q = candidate_tree(rng, spec[0], spec[1], quantum)
+        parents.append(p)
+        probs.append(q)
+    offs = np.concatenate([[0], np.cumsum([p.size for p in parents])]).astype(np.int32)
+    return offs, np.concatenate(parents), np.concatenate(probs)
