@@ -332,6 +332,99 @@ def conv_leg(args, cfg, log):
     }
 
 
+def budget_bytes(M, B, N):
+    """tree_budget_select: candidate parents and probabilities read once, rho
+    and rank written once, node_offsets written, parent and src written per
+    packed node (the hand-offs between its three launches stay in L2)."""
+    return 8 * M + 8 * M + 4 * (B + 1) + 8 * N
+
+
+def budget_leg(args, log):
+    """Times tree_budget_select (the batch-wide allocation and the forest
+    materialiser) on the candidate batch shaped after the chosen config."""
+    import torch
+    from paper_2608_01651_amd import treelin as tl
+    from synth import workloads as W
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU (HIP) device")
+    tl.lib()
+    case = W.budget_case(args.workload)
+    offs, par, prob = W.make_candidates(args.seed, case.sizes)
+    B, M = len(case.sizes), int(offs[-1])
+    dev = "cuda:0"
+    i32 = dict(dtype=torch.int32, device=dev)
+    t_offs = torch.from_numpy(offs.astype(np.int32)).to(dev)
+    t_par = torch.from_numpy(par.astype(np.int32)).to(dev)
+    t_prob = torch.from_numpy(prob.astype(np.float32)).to(dev)
+    rho = torch.empty(M, dtype=torch.float32, device=dev)
+    rank = torch.empty(M, **i32)
+    no = torch.empty(B + 1, **i32)
+    fpar = torch.empty(case.capacity, **i32)
+    src = torch.empty(case.capacity, **i32)
+    err = torch.zeros(1, **i32)
+    prob_t = tl.problem(B, 1, 1, 16, 16, case.max_nodes)
+    log(f"budget allocation: {args.workload} B={B} candidates={M} capacity={case.capacity} "
+        f"max_nodes={case.max_nodes}")
+
+    def run():
+        tl.budget_select(prob_t, M, case.capacity, t_offs, t_par, t_prob, rho, rank, no, fpar, src,
+                         dev_err=err)
+
+    for _ in range(max(1, args.warmup)):
+        run()
+    torch.cuda.synchronize()
+    replay = run
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            run()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph):
+            run()
+        torch.cuda.synchronize()
+        replay = graph.replay
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        replay()
+    end.record()
+    torch.cuda.synchronize()
+    if err.item() != 0:
+        raise RuntimeError(f"device error {tl.status_string(err.item())}")
+    N = int(no[-1].item())
+    us = start.elapsed_time(end) * 1e3 / args.steps
+    nbytes = budget_bytes(M, B, N)
+    achieved = nbytes / (us * 1e-6) / 1e9
+    out = {
+        "metric": "batch-wide budget allocation + forest materialisation: candidates/s (1 MI355X)",
+        "value": round(M / (us * 1e-6), 1), "unit": "candidates/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "us_per_allocation": round(us, 3),
+        "higher_is_better": True, "dtype": "f32 scores, int32 indices", "data": "synthetic",
+        "graph": bool(args.graph),
+        "config": {"workload": f"{args.workload} candidate batch: B={B}, {M} candidates, "
+                               f"capacity {case.capacity}, max_nodes {case.max_nodes}",
+                   "selected": N},
+        "roofline": {"bound": "latency", "kernel": "tree_budget_select (3 launches)",
+                     "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 5), "algorithmic_bytes": int(nbytes)},
+    }
+    if not args.no_cpu_baseline:
+        import time
+        import oracle
+        reps, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < min(args.cpu_seconds, 5.0):
+            oracle.budget_select(offs, par, prob, case.capacity, case.max_nodes)
+            reps += 1
+        dt = (time.perf_counter() - t0) / reps
+        out["cpu_baseline"] = {"value": round(M / dt, 1), "unit": "candidates/s", "cores": 1,
+                               "kind": "oracle", "sample": f"{reps} whole allocations of this batch"}
+    return out
+
+
 # ---------------------------------------------------------------------------
 # CPU baseline: the fp64 oracle on a bounded sample of the same workload
 # ---------------------------------------------------------------------------
@@ -465,6 +558,8 @@ def main():
     ap.add_argument("--conv", action="store_true",
                     help="time the tree-parallel convolution front end (tree_conv_gates) instead")
     ap.add_argument("--conv-width", type=int, default=4)
+    ap.add_argument("--budget", action="store_true",
+                    help="time the batch-wide budget allocation (tree_budget_select) instead")
     ap.add_argument("--graph", action="store_true",
                     help="capture one round of launches in a HIP graph and time its replays")
     ap.add_argument("--commit-layers", action="store_true",
@@ -490,6 +585,9 @@ def main():
     cfg = W.CONFIGS[args.workload]
     if args.conv:
         print(json.dumps(conv_leg(args, cfg, log)), flush=True)
+        return
+    if args.budget:
+        print(json.dumps(budget_leg(args, log)), flush=True)
         return
     cpu = None
     if not args.no_cpu_baseline:

@@ -228,6 +228,49 @@ tl_status tree_conv_state_commit(const tl_problem* problem, int32_t conv_width,
                                  void* conv_state, const int32_t* slot,
                                  int32_t* dev_err, void* stream);
 
+/* Batch-wide verification-budget allocation and forest materialiser (§5.1
+ * "Batch-wide utility allocation"; the packed forest of §5.2).
+ *
+ * Input: per request b a drafter's candidate tree of M_b nodes (parents
+ * before children, -1 for a root) with the draft probability p(u | parent(u))
+ * of every node, in [0, 1].  Computes
+ *   rho(v) = p(root) * ... * p(v) along v's root path, in fp32, root first,
+ *            one rounding per step;
+ *   rank(v) = v's position among its request's non-root candidates in the
+ *            order (rho descending, index ascending); -1 for roots.
+ * Every root is kept; K = capacity - (all roots) further nodes are the first
+ * K eligible candidates of the batch in the order (rho descending, batch-wide
+ * index ascending), where a candidate is eligible while rank(v) <
+ * max_nodes - (roots of its request), so no request exceeds max_nodes.  The
+ * selected nodes of each request form a prefix-connected subtree; they are
+ * packed request by request in candidate order:
+ *   node_offsets [B+1]: the per-request budgets' exclusive scan (sum <= capacity);
+ *   parent [N]: request-local parent of each packed node in packed numbering;
+ *   src [N]: batch-wide candidate index of each packed node,
+ * so that node_offsets and parent are tree_lin_attn_verify's forest and src
+ * gathers its per-node rows.  Entries past node_offsets[B] are not written.
+ * Layouts: cand_offsets [B+1] (cand_offsets[0] = 0, non-decreasing,
+ *   cand_offsets[B] <= num_candidates), cand_parent [num_candidates] int32
+ *   request-local, cand_prob [num_candidates] fp32; rho, rank
+ *   [num_candidates]; parent, src [capacity].  Only batch and max_nodes of
+ *   `problem` are used (the rest is checked as for tree_lin_attn_verify).
+ * Bounds: B <= 1024, M_b <= 1024, num_candidates <= 32768 (TL_EUNSUPPORTED
+ *   on the host; a device size beyond them is TL_EINVAL).
+ * Device errors: TL_EBADTREE (offsets), TL_EINVAL (a request with more than
+ *   1024 candidates or more roots than max_nodes, capacity below the roots):
+ *   nothing is selected and node_offsets is all zero.  Per request,
+ *   TL_EBADTREE (a bad parent) or TL_EINVAL (a probability outside [0, 1]):
+ *   that request keeps only its roots, its rho and rank are unspecified.
+ * node_offsets[1..B] also carries a count between the launches, so it must
+ * not alias the candidate arrays. */
+tl_status tree_budget_select(const tl_problem* problem, int32_t num_candidates, int32_t capacity,
+                             const int32_t* cand_offsets, const int32_t* cand_parent,
+                             const float* cand_prob,
+                             float* rho, int32_t* rank,     /* [num_candidates] out */
+                             int32_t* node_offsets,         /* [B+1] out */
+                             int32_t* parent, int32_t* src, /* [capacity] out */
+                             int32_t* dev_err, void* stream);
+
 /* Tree topology of §4.1's notation table, as the kernels build it:
  * anc_mask[r, w] (W = ceil(max_nodes/64) uint64 words per node) has bit
  * (j mod 64) of word j/64 set iff local node j is r's node itself or one of

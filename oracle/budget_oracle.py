@@ -32,6 +32,8 @@ Readings (the paper leaves these open; the design notes list them)
   max_nodes - (roots of its request) among its request's non-root
   candidates, i.e. the greedy selection skips a request once it is full.
 * The capacity must cover every root of every request with candidates.
+* Draft probabilities lie in [0, 1]: that bound is what keeps a child's rho
+  at or below its parent's, so a value outside it (or NaN) is rejected.
 """
 from __future__ import annotations
 
@@ -48,6 +50,8 @@ def path_scores(cand_parent, cand_prob):
         p = int(cand_parent[v])
         if not (p == -1 or 0 <= p < v):
             raise BadTree(f"candidate {v}: parent {p} is not -1 or in [0,{v})")
+        if not (0.0 <= float(cand_prob[v]) <= 1.0):
+            raise InvalidArg(f"candidate {v}: probability {cand_prob[v]} is outside [0, 1]")
         rho[v] = cand_prob[v] if p == -1 else np.float32(rho[p] * np.float32(cand_prob[v]))
     return rho
 

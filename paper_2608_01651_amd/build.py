@@ -22,7 +22,8 @@ LIB = os.path.join(PKG, "libtreelin.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["verify.hip", "verify_tiled.hip", "commit.hip", "topology.hip", "conv.hip", "abi.cpp"]
+SOURCES = ["verify.hip", "verify_tiled.hip", "commit.hip", "topology.hip", "conv.hip", "budget.hip",
+           "abi.cpp"]
 COMMON = ["-std=c++17", "-O3", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}",
           "-Wall", "-Wno-unused-function"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

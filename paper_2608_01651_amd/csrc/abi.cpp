@@ -282,6 +282,45 @@ tl_status tree_conv_state_commit(const tl_problem* problem, int32_t conv_width,
   return tl::launch_conv_state_commit(a, conv_width, reinterpret_cast<hipStream_t>(stream));
 }
 
+tl_status tree_budget_select(const tl_problem* problem, int32_t num_candidates, int32_t capacity,
+                             const int32_t* cand_offsets, const int32_t* cand_parent,
+                             const float* cand_prob, float* rho, int32_t* rank,
+                             int32_t* node_offsets, int32_t* parent, int32_t* src,
+                             int32_t* dev_err, void* stream) {
+  tl_status st = check_problem(problem);
+  if (st != TL_OK) return st;
+  if (problem->batch == 0) return TL_OK;
+  if (num_candidates < 0 || capacity < 0) return TL_EINVAL;
+  if (problem->batch > tl::kBudgetMaxBatch || num_candidates > tl::kBudgetMaxCandidates)
+    return TL_EUNSUPPORTED;
+  if (!cand_offsets || !cand_parent || !cand_prob || !rho || !rank || !node_offsets || !parent ||
+      !src)
+    return TL_EINVAL;
+  if (!aligned(cand_offsets, 4) || !aligned(cand_parent, 4) || !aligned(cand_prob, 4) ||
+      !aligned(rho, 4) || !aligned(rank, 4) || !aligned(node_offsets, 4) || !aligned(parent, 4) ||
+      !aligned(src, 4))
+    return TL_EINVAL;
+  if (dev_err && !aligned(dev_err, 4)) return TL_EINVAL;
+  tl::BudgetArgs a;
+  a.cand_offsets = cand_offsets;
+  a.cand_parent = cand_parent;
+  a.cand_prob = cand_prob;
+  a.rho = rho;
+  a.rank = rank;
+  a.node_offsets = node_offsets;
+  a.parent = parent;
+  a.src = src;
+  a.dev_err = dev_err;
+  a.batch = problem->batch;
+  a.max_nodes = problem->max_nodes;
+  a.num_candidates = num_candidates;
+  a.capacity = capacity;
+#ifdef TL_TRACE
+  a.trace = g_trace;
+#endif
+  return tl::launch_budget_select(a, reinterpret_cast<hipStream_t>(stream));
+}
+
 const char* tl_status_string(tl_status s) {
   switch (s) {
     case TL_OK: return "TL_OK: success";

@@ -131,6 +131,28 @@ struct ConvCommitArgs {
   int batch, C, max_nodes, num_slots, tiles;
 };
 
+// tree_budget_select
+constexpr int kBudgetMaxTree = 1024;          // candidates per request (one per thread)
+constexpr int kBudgetMaxBatch = 1024;         // requests (one per selection thread)
+constexpr int kBudgetMaxCandidates = 32768;   // candidates per batch (one workgroup's LDS)
+constexpr int kSelectThreads = 1024;
+
+struct BudgetArgs {
+  const int32_t* cand_offsets;
+  const int32_t* cand_parent;
+  const float* cand_prob;
+  float* rho;
+  int32_t* rank;
+  int32_t* node_offsets;
+  int32_t* parent;
+  int32_t* src;
+  int32_t* dev_err;
+  int batch, max_nodes, num_candidates, capacity;
+#ifdef TL_TRACE
+  long long* trace;  // [blocks][16] wall-clock stamps (trace builds only)
+#endif
+};
+
 tl_status launch_verify(const tl_problem& p, const VerifyArgs& a, hipStream_t stream);
 tl_status launch_verify_tiled(const tl_problem& p, const VerifyArgs& a, hipStream_t stream);
 int verify_tiled_lds_bytes(int mode, int d, int tm, int W);
@@ -140,6 +162,8 @@ tl_status launch_accepted_path(const PathArgs& a, hipStream_t stream);
 tl_status launch_topology(const TopoArgs& a, hipStream_t stream);
 tl_status launch_conv_gates(const ConvArgs& a, int width, bool gdn, hipStream_t stream);
 tl_status launch_conv_state_commit(const ConvCommitArgs& a, int width, hipStream_t stream);
+tl_status launch_budget_select(const BudgetArgs& a, hipStream_t stream);
+int budget_select_lds_bytes(int batch, int num_candidates);
 int verify_lds_bytes(const tl_problem& p, int tm);
 
 }  // namespace tl

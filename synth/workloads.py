@@ -457,3 +457,39 @@ def make_candidates(seed, sizes, quantum=None):
         probs.append(q)
     offs = np.concatenate([[0], np.cumsum([p.size for p in parents])]).astype(np.int32)
     return offs, np.concatenate(parents), np.concatenate(probs)
+
+
+@dataclasses.dataclass
+class BudgetCase:
+    """A batch-wide allocation workload: per-request candidate-tree specs
+    (branching, depth_cap) or None, the batch capacity and the per-request
+    node bound."""
+    sizes: list
+    capacity: int
+    max_nodes: int
+
+
+def budget_case(name):
+    """Candidate batches shaped after the verification configs: each request
+    drafts several times the nodes its share of the capacity can verify, and
+    the capacity is the config's batch x tree size.
+      tiny:       1 request, binary tree of depth 4 (31 candidates), capacity 15
+      mid:        1 request, branching 4,4,2 to depth 8 (213), capacity 64
+      production: 32 requests, branching 8,4,2 to depth 10 (553 each), capacity 2048
+                  (32 x 64), max_nodes 128, so budgets vary between requests
+      gdn:        16 requests, branching 16,4,2 to depth 8 (849 each), capacity 2048
+                  (16 x 128), max_nodes 256
+      large:      128 requests of mixed trees (branching 4,2,2 / 2,2,2 / 8,2 / a
+                  chain of 16; 16-237 candidates), capacity 8192, max_nodes 256"""
+    if name == "tiny":
+        return BudgetCase([((2, 2, 2, 2), 4)], 15, 16)
+    if name == "mid":
+        return BudgetCase([((4, 4, 2), 8)], 64, 64)
+    if name == "production":
+        return BudgetCase([((8, 4, 2), 10)] * 32, 32 * 64, 128)
+    if name == "gdn":
+        return BudgetCase([((16, 4, 2), 8)] * 16, 16 * 128, 256)
+    if name == "large":
+        kinds = [((4, 2, 2), 16), ((2, 2, 2), 12), ((8, 2), 10), ((1,), 15)]
+        return BudgetCase([kinds[b % 4] for b in range(128)], 8192, 256)
+    raise KeyError(name)

@@ -34,7 +34,7 @@ def test_library_exports_every_declared_function():
     names = _declared_functions()
     assert {"tree_lin_attn_verify", "tree_state_commit", "tree_topology_export",
             "tree_state_commit_layers", "tree_accepted_path", "tree_conv_gates",
-            "tree_conv_state_commit",
+            "tree_conv_state_commit", "tree_budget_select",
             "tl_status_string", "tl_version"} <= set(names)
     for n in names:
         assert hasattr(L, n), f"{n} declared in include/treelin.h but not exported"
@@ -121,6 +121,7 @@ def P(**kw):
     (P(num_slots=0), tl.TL_EINVAL),
 ])
 def test_problem_checks(prob, code):
+    assert _budget(prob) == code
     assert _verify(prob) == code
     assert _commit(prob) == code
     assert _topology(prob) == code
@@ -236,3 +237,23 @@ def test_conv_entry_points_checks():
         assert _conv_commit(P(), **{field: None}) == tl.TL_EINVAL, field
     assert _conv_commit(P(), x=A16 + 4) == tl.TL_EINVAL
     assert _conv_commit(P(batch=0), offs=None) == tl.TL_OK
+
+
+def _budget(prob, num_candidates=64, capacity=16, **kw):
+    f = dict(offs=A16, cpar=A16, cprob=A16, rho=A16, rank=A16, no=A16, par=A16, src=A16, err=None)
+    f.update(kw)
+    return _lib_or_build().tree_budget_select(
+        None if prob is None else ctypes.byref(prob), num_candidates, capacity, f["offs"], f["cpar"],
+        f["cprob"], f["rho"], f["rank"], f["no"], f["par"], f["src"], f["err"], None)
+
+
+def test_budget_select_checks():
+    assert _budget(P(batch=0), offs=None, src=None) == tl.TL_OK
+    assert _budget(P(), num_candidates=-1) == tl.TL_EINVAL
+    assert _budget(P(), capacity=-1) == tl.TL_EINVAL
+    assert _budget(P(batch=1025)) == tl.TL_EUNSUPPORTED
+    assert _budget(P(), num_candidates=32769) == tl.TL_EUNSUPPORTED
+    for field in ("offs", "cpar", "cprob", "rho", "rank", "no", "par", "src"):
+        assert _budget(P(), **{field: None}) == tl.TL_EINVAL, field
+        assert _budget(P(), **{field: MIS}) == tl.TL_EINVAL, field
+    assert _budget(P(), err=MIS) == tl.TL_EINVAL

@@ -130,6 +130,11 @@ def test_errors():
         oracle.budget_select(offs, bad, prob, 6, 64)
     with pytest.raises(oracle.InvalidArg):
         oracle.budget_select(offs, parent, prob, 1, 64)            # two roots, capacity 1
+    for bad_p in (1.5, -0.25, float("nan")):                       # not a probability
+        bp = prob.copy()
+        bp[2] = bad_p
+        with pytest.raises(oracle.InvalidArg):
+            oracle.budget_select(offs, parent, bp, 6, 64)
 
 
 def test_pins_reject_a_flipped_tie_break(monkeypatch):

@@ -1,0 +1,302 @@
+"""GPU parity of the batch-wide budget allocation and forest materialiser
+(tree_budget_select, §5.1-§5.2) against the oracle (oracle/budget_oracle.py),
+through the C ABI.
+
+Everything here is integer or bit-level: rho is compared bit for bit (both
+sides form it in fp32, root first, one rounding per step), ranks, budgets,
+packed parents and source rows exactly."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import workloads as W
+from tests import gpu_helpers as H
+from paper_2608_01651_amd import treelin as tl
+
+pytestmark = pytest.mark.gpu
+
+NAMES = ["tiny", "mid", "production", "gdn", "large"]
+
+
+class Bufs:
+    """Device buffers of one allocation call; num_candidates and capacity fix
+    the bucket."""
+
+    def __init__(self, B, num_candidates, capacity):
+        dev = H.dev()
+        self.B, self.nc, self.cap = B, num_candidates, capacity
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.offs = torch.zeros(B + 1, **i32)
+        self.cpar = torch.zeros(max(num_candidates, 1), **i32)
+        self.cprob = torch.zeros(max(num_candidates, 1), dtype=torch.float32, device=dev)
+        self.rho = torch.zeros(max(num_candidates, 1), dtype=torch.float32, device=dev)
+        self.rank = torch.zeros(max(num_candidates, 1), **i32)
+        self.no = torch.zeros(B + 1, **i32)
+        self.parent = torch.zeros(max(capacity, 1), **i32)
+        self.src = torch.zeros(max(capacity, 1), **i32)
+        self.err = torch.zeros(1, **i32)
+
+    def load(self, offs, par, prob):
+        """Eager copies of a new candidate batch; outputs poisoned."""
+        M = int(offs[-1]) if len(offs) else 0
+        self.offs.copy_(torch.from_numpy(np.asarray(offs, np.int32)))
+        if M:
+            self.cpar[:M].copy_(torch.from_numpy(np.asarray(par, np.int32)))
+            self.cprob[:M].copy_(torch.from_numpy(np.asarray(prob, np.float32)))
+        self.rho.fill_(float("nan"))
+        self.rank.fill_(-7)
+        self.no.fill_(-7)
+        self.parent.fill_(-7)
+        self.src.fill_(-7)
+        self.err.zero_()
+
+    def launch(self, max_nodes):
+        prob = tl.problem(self.B, 1, 1, 16, 16, max_nodes)
+        tl.budget_select(prob, self.nc, self.cap, self.offs, self.cpar, self.cprob, self.rho,
+                         self.rank, self.no, self.parent, self.src, dev_err=self.err)
+
+    def result(self):
+        torch.cuda.synchronize()
+        M = int(self.offs[-1].item())
+        N = int(self.no[-1].item())
+        return dict(rho=self.rho[:M].cpu().numpy(), rank=self.rank[:M].cpu().numpy(),
+                    node_offsets=self.no.cpu().numpy(), parent=self.parent[:N].cpu().numpy(),
+                    src=self.src[:N].cpu().numpy(), err=int(self.err.item()))
+
+
+def run(offs, par, prob, capacity, max_nodes, num_candidates=None):
+    offs = np.asarray(offs, np.int32)
+    M = int(offs[-1])
+    bufs = Bufs(len(offs) - 1, M if num_candidates is None else num_candidates, capacity)
+    bufs.load(offs, par, prob)
+    bufs.launch(max_nodes)
+    return bufs.result()
+
+
+def assert_same(got, ref, what=""):
+    assert got["err"] == 0, what
+    np.testing.assert_array_equal(got["rho"].view(np.uint32), ref["rho"].view(np.uint32), err_msg=what)
+    np.testing.assert_array_equal(got["rank"], ref["rank"], err_msg=what)
+    np.testing.assert_array_equal(got["node_offsets"], ref["node_offsets"], err_msg=what)
+    np.testing.assert_array_equal(got["parent"], ref["parent"], err_msg=what)
+    np.testing.assert_array_equal(got["src"], ref["src"], err_msg=what)
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_budget_parity(name):
+    case = W.budget_case(name)
+    offs, par, prob = W.make_candidates(3, case.sizes)
+    print(f"budget {name}: B={len(case.sizes)} M={int(offs[-1])} capacity={case.capacity}", flush=True)
+    got = run(offs, par, prob, case.capacity, case.max_nodes)
+    ref = oracle.budget_select(offs, par, prob, case.capacity, case.max_nodes)
+    assert_same(got, ref, name)
+    assert int(got["node_offsets"][-1]) == case.capacity   # the drafts always cover the capacity
+
+
+@pytest.mark.parametrize("quantum", [None, 1 / 16, 1 / 64])
+@pytest.mark.parametrize("max_nodes", [4, 16, 256])
+def test_budget_ties_caps_and_capacities(quantum, max_nodes):
+    """Quantised probabilities make many equal rho (ties across requests
+    decide by batch-wide index); a small max_nodes makes requests fill up;
+    capacities from the roots alone (K = 0) to more than every eligible node."""
+    sizes = [((3, 2), 5), None, ((4, 2, 1), 6), ((2,), 9), ((5, 3), 4), None, ((2, 2, 2), 7)]
+    offs, par, prob = W.make_candidates(11, sizes, quantum=quantum)
+    roots = int((par == -1).sum())
+    for capacity in (roots, roots + 1, roots + 7, roots + 40, roots + 150, int(offs[-1]) + 5):
+        print(f"ties q={quantum} max_nodes={max_nodes} capacity={capacity}", flush=True)
+        got = run(offs, par, prob, capacity, max_nodes)
+        ref = oracle.budget_select(offs, par, prob, capacity, max_nodes)
+        assert_same(got, ref, f"capacity {capacity}")
+
+
+def forest_batch(parts):
+    """(parent, prob) per request -> cand_offsets, parent, prob."""
+    offs = np.concatenate([[0], np.cumsum([len(p) for p, _ in parts])]).astype(np.int32)
+    par = np.concatenate([np.asarray(p, np.int32) for p, _ in parts]) if parts else np.zeros(0, np.int32)
+    prob = np.concatenate([np.asarray(q, np.float32) for _, q in parts]) if parts else np.zeros(0, np.float32)
+    return offs, par, prob
+
+
+def test_budget_edge_trees():
+    """A 1024-deep chain (1024 Jacobi sweeps), a 1024-candidate star (the
+    largest sort), a multi-root forest, a single root, empty requests, and
+    probabilities of 0, 1 and denormal products."""
+    rng = np.random.default_rng(5)
+    chain = (np.arange(-1, 1023, dtype=np.int32), rng.uniform(0.97, 1.0, 1024).astype(np.float32))
+    star = (np.r_[-1, np.zeros(1023, np.int32)], rng.uniform(0, 1, 1024).astype(np.float32))
+    forest = (np.array([-1, 0, -1, 2, 1, -1, 5, 3, 3], np.int32),
+              np.array([1, .5, .25, 1, .5, 1e-20, 1e-20, 0, 1], np.float32))
+    single = (np.array([-1], np.int32), np.array([0.5], np.float32))
+    empty = (np.zeros(0, np.int32), np.zeros(0, np.float32))
+    offs, par, prob = forest_batch([empty, chain, forest, empty, star, single, empty])
+    for capacity, max_nodes in ((6, 256), (40, 256), (300, 256), (700, 256), (5000, 256), (600, 64)):
+        print(f"edge capacity={capacity} max_nodes={max_nodes}", flush=True)
+        got = run(offs, par, prob, capacity, max_nodes)
+        ref = oracle.budget_select(offs, par, prob, capacity, max_nodes)
+        assert_same(got, ref, f"capacity {capacity}")
+
+
+def test_budget_empty_batch_and_no_candidates():
+    got = run([0, 0, 0], [], [], 4, 16)
+    assert got["err"] == 0
+    np.testing.assert_array_equal(got["node_offsets"], [0, 0, 0])
+
+
+def test_budget_bucket_larger_than_the_batch():
+    """num_candidates and capacity are buffer extents of a bucket: a smaller
+    batch inside them gives the oracle's result for that capacity."""
+    case = W.budget_case("production")
+    offs, par, prob = W.make_candidates(4, case.sizes[:5])
+    got = run(offs, par, prob, 5 * 64 + 100, case.max_nodes, num_candidates=int(offs[-1]) + 999)
+    assert_same(got, oracle.budget_select(offs, par, prob, 5 * 64 + 100, case.max_nodes))
+
+
+def per_request_ref(offs, par, prob, b):
+    o0, o1 = int(offs[b]), int(offs[b + 1])
+    return oracle.budget_select([0, o1 - o0], par[o0:o1], prob[o0:o1], 10 ** 6, 10 ** 6)
+
+
+@pytest.mark.parametrize("kind", ["parent", "prob_high", "prob_nan"])
+def test_budget_bad_request_keeps_only_its_roots(kind):
+    sizes = [((3, 2), 5), ((4, 2), 4), ((2, 2), 6)]
+    offs, par, prob = W.make_candidates(8, sizes)
+    par, prob = par.copy(), prob.copy()
+    o1 = int(offs[1])
+    if kind == "parent":
+        par[o1 + 6] = 9                                   # a parent after its child
+        code = tl.TL_EBADTREE
+    else:
+        prob[o1 + 6] = 1.5 if kind == "prob_high" else np.nan
+        code = tl.TL_EINVAL
+    par[o1 + 2] = -1                                      # and a second root
+    got = run(offs, par, prob, 30, 64)
+    assert got["err"] == code
+    no = got["node_offsets"]
+    # the bad request: its roots, in order, nothing else
+    roots = [o1 + v for v in range(int(offs[2]) - o1) if par[o1 + v] == -1]
+    np.testing.assert_array_equal(got["src"][no[1]:no[2]], roots)
+    np.testing.assert_array_equal(got["parent"][no[1]:no[2]], -1)
+    assert int(no[-1]) == 30
+    # the good requests: their rho and ranks, and a prefix of their order
+    for b in (0, 2):
+        r = per_request_ref(offs, par, prob, b)
+        sl = slice(int(offs[b]), int(offs[b + 1]))
+        np.testing.assert_array_equal(got["rho"][sl].view(np.uint32), r["rho"].view(np.uint32))
+        np.testing.assert_array_equal(got["rank"][sl], r["rank"])
+        take = int(no[b + 1] - no[b]) - 1                 # one root each
+        want = [int(offs[b]) + v for v in range(sl.stop - sl.start)
+                if r["rank"][v] < take]                   # root's rank is -1
+        np.testing.assert_array_equal(got["src"][no[b]:no[b + 1]], want)
+
+
+def test_budget_batch_errors_select_nothing():
+    sizes = [((3, 2), 4), ((2, 2), 4)]
+    offs, par, prob = W.make_candidates(2, sizes)
+    M = int(offs[-1])
+    cases = []
+    cases.append(("capacity below the roots", offs, par, prob, 1, 64, M, tl.TL_EINVAL))
+    cases.append(("decreasing offsets", np.array([0, M, M - 3], np.int32), par, prob, 20, 64, M,
+                  tl.TL_EBADTREE))
+    cases.append(("offsets start above 0", np.array([2, offs[1], M], np.int32), par, prob, 20, 64, M,
+                  tl.TL_EBADTREE))
+    cases.append(("offsets past num_candidates", offs, par, prob, 20, 64, M - 1, tl.TL_EINVAL))
+    many = np.full(3, -1, np.int32)
+    cases.append(("more roots than max_nodes", np.array([0, 3], np.int32), many, np.ones(3, np.float32),
+                  20, 2, 3, tl.TL_EINVAL))
+    big = np.r_[-1, np.zeros(1024, np.int32)]
+    cases.append(("1025 candidates", np.array([0, 1025], np.int32), big, np.full(1025, .5, np.float32),
+                  20, 64, 1025, tl.TL_EINVAL))
+    for what, o, p, q, cap, mn, nc, code in cases:
+        print(f"batch error: {what}", flush=True)
+        bufs = Bufs(len(o) - 1, nc, cap)
+        bufs.offs.copy_(torch.from_numpy(np.asarray(o, np.int32)))
+        n = min(nc, len(p))
+        bufs.cpar[:n].copy_(torch.from_numpy(np.asarray(p[:n], np.int32)))
+        bufs.cprob[:n].copy_(torch.from_numpy(np.asarray(q[:n], np.float32)))
+        bufs.no.fill_(-7)
+        bufs.src.fill_(-7)
+        bufs.err.zero_()
+        bufs.launch(mn)
+        torch.cuda.synchronize()
+        assert int(bufs.err.item()) == code, what
+        assert torch.all(bufs.no == 0).item(), what
+        assert torch.all(bufs.src == -7).item(), what
+
+
+def test_budget_graph_replay():
+    """One captured allocation replayed over rounds of new candidate batches
+    in the same buffers (fixed B, num_candidates and capacity); each replay is
+    checked against the oracle, with eager work between replays."""
+    B, nc, cap, max_nodes = 8, 8 * 400, 8 * 48, 64
+    bufs = Bufs(B, nc, cap)
+
+    def round_batch(rnd):
+        rng = np.random.default_rng([rnd, 31])
+        sizes = []
+        for b in range(B):
+            if (rnd + b) % 5 == 4:
+                sizes.append(None)
+            else:
+                sizes.append(((int(rng.integers(2, 8)), 2, 2), int(rng.integers(3, 9))))
+        o, p, q = W.make_candidates(100 + rnd, sizes, quantum=1 / 32 if rnd % 2 else None)
+        assert int(o[-1]) <= nc, int(o[-1])
+        return o, p, q
+
+    bufs.load(*round_batch(0))
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        bufs.launch(max_nodes)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        bufs.launch(max_nodes)
+    torch.cuda.synchronize()
+    scratch = torch.randn(1 << 16, device=H.dev())
+    for rnd in range(1, 6):
+        o, p, q = round_batch(rnd)
+        bufs.load(o, p, q)
+        graph.replay()
+        got = bufs.result()
+        ref = oracle.budget_select(o, p, q, cap, max_nodes)
+        assert_same(got, ref, f"round {rnd}")
+        scratch.mul_(0.5).add_(1.0)                       # eager work between replays
+        torch.cuda.synchronize()
+
+
+def test_budget_feeds_verification():
+    """The materialised forest is verify's input: gather the selected rows by
+    src and verify them; the result equals the oracle on the same forest."""
+    cfg = W.CONFIGS["production"]
+    case = W.budget_case("production")
+    B = 4
+    offs, par, prob = W.make_candidates(6, case.sizes[:B])
+    cap = B * cfg.max_nodes
+    got = run(offs, par, prob, cap, cfg.max_nodes)
+    assert got["err"] == 0
+    no, fpar, src = got["node_offsets"], got["parent"], got["src"]
+    N = int(no[-1])
+    # per-candidate rows (one synthetic row per candidate), gathered by src
+    rng = np.random.default_rng(12)
+    M = int(offs[-1])
+    Hk, Hv, d = cfg.num_qk_heads, cfg.num_v_heads, cfg.d_k
+    kq = rng.standard_normal((M, 2, Hk, d)).astype(np.float32)
+    kq /= np.linalg.norm(kq, axis=-1, keepdims=True)
+    q_all, k_all = W.round_bf16(kq[:, 0]), W.round_bf16(kq[:, 1])
+    v_all = W.round_bf16(rng.standard_normal((M, Hv, d)).astype(np.float32))
+    g_all = (-np.logaddexp(0, rng.standard_normal((M, Hv)) - 2)).astype(np.float32)
+    q, k, v, g = q_all[src], k_all[src], v_all[src], g_all[src]
+    state = (0.1 * rng.standard_normal((B, Hv, d, d))).astype(np.float32)
+    dev = H.dev()
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(torch.bfloat16)
+    out = torch.full((N, Hv, d), float("nan"), device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    tl.verify(H.problem_for(cfg, B), H.t_int(no), H.t_int(fpar), bf(q), bf(k), bf(v), H.t_f32(g), None,
+              H.t_f32(state), out, dev_err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    ref = oracle.verify(cfg.mode, Hk, no, fpar, q, k, v, g, None, state, q_scale=cfg.q_scale,
+                        max_nodes=cfg.max_nodes)
+    assert H.slice_rel_err(out.cpu().numpy(), ref, no) < H.TOL
