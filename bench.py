@@ -70,16 +70,23 @@ def conv_bytes(cfg, N, B, width):
     return N * per_node + B * (width - 1) * C * 2 + C * (width + 1) * 4 + 2 * Hv * 4 + 4 * (B + 1)
 
 
+# The sources that the verify and commit launches of the benchmark compile from.
+HASHED_SOURCES = ["include/treelin.h"] + [
+    "paper_2608_01651_amd/csrc/" + f for f in
+    ("tl_device.h", "tl_kernels.h", "verify_common.h", "verify_gdn.h", "verify_gla_small.h",
+     "verify_vector.h", "verify.hip", "commit.hip")]
+
+
 def source_hash():
-    """Hash of the kernel sources' code: comments and whitespace are dropped,
-    so that only a change to what is compiled invalidates stored counters."""
+    """Hash of the verify and commit kernels' source code: comments and
+    whitespace are dropped, so that only a change to what those kernels
+    compile from invalidates stored counters."""
     h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2608_01651_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        with open(os.path.join(csrc, f), encoding="utf-8") as fh:
+    for f in HASHED_SOURCES:
+        with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
             code = re.sub(r"/\*.*?\*/", " ", fh.read(), flags=re.S)
         code = re.sub(r"//[^\n]*", " ", code)
-        h.update(f.encode() + " ".join(code.split()).encode())
+        h.update(os.path.basename(f).encode() + " ".join(code.split()).encode())
     return h.hexdigest()[:16]
 
 

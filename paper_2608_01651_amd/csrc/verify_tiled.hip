@@ -309,79 +309,96 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     return (unsigned)(s_tmask[I * W + (c >> 1)] >> ((c & 1) * 32));
   };
 
-  // 1. coefficient chunks of tile I, shared over the waves, into buffer buf
+  // 1. coefficient chunks of tile I, shared over the waves, into buffer buf.
+  // The work is dealt out by half-chunk (one 16-node tile J each), so that a
+  // wave carries at most one half-chunk per node tile (NW >= 8 at d = 128).
   auto chunks = [&](int I, const bf16x8 (&qf)[KS], const TileIn& t, unsigned char* buf, float* gin)
                     __attribute__((always_inline)) {
-    const int nc = I / 2 + 1;
+    const int nh = 2 * (I / 2 + 1);   // tiles 0 .. 2 (I / 2) + 1: whole chunks
     const int i = kTile * I + lr;
-    bf16x8 kfi[KS];
-    if constexpr (GDN) {
+    for (int J = wave; J < nh; J += NW) {   // uniform
+      const int c = J >> 1, hf = J & 1;
+      const unsigned bits = (tile_bits32(I, c) >> (hf * kTile)) & 0xFFFFu;
+      float cv[4] = {0.f, 0.f, 0.f, 0.f}, gv[4] = {0.f, 0.f, 0.f, 0.f};
+      if (J <= I && bits) {   // uniform
+        bf16x8 kj[KS], kfi[KS];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kfi[ks] = kfrag(kTile * I, ks);
-    }
-    for (int c = wave; c < nc; c += NW) {
-      uint32_t cw[2][4], gw[2][4];   // per half: hi01 hi23 lo01 lo23
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        const int J = 2 * c + hf;
-        const unsigned bits = (tile_bits32(I, c) >> (hf * kTile)) & 0xFFFFu;
-        float cv[4] = {0.f, 0.f, 0.f, 0.f}, gv[4] = {0.f, 0.f, 0.f, 0.f};
-        if (J <= I && bits) {   // uniform
-          f32x4 qk = f32x4{0.f, 0.f, 0.f, 0.f}, kk = qk;
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks) {
-            const bf16x8 kj = kfrag(kTile * J, ks);
-            qk = mfma16(kj, qf[ks], qk);               // rows j, column i: k_j . q_i
-            if constexpr (GDN) kk = mfma16(kj, kfi[ks], kk);
-          }
-          const uint64_t mw = (i < T) ? s_mask[i * W + (J >> 2)] : 0ull;   // M+ row of node i
-          const unsigned mb = (unsigned)(mw >> ((J & 3) * kTile + 4 * lg)) & 0xFu;
-          const f32x4 clj = *reinterpret_cast<const f32x4*>(s_cl + kTile * J + 4 * lg);
-          const unsigned self = (J == I) ? (1u << lr) >> (4 * lg) : 0u;   // bit r: j == i
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const bool m = (mb >> r) & 1u;
-            const float dec = __builtin_amdgcn_exp2f(t.cli - clj[r]);
-            cv[r] = m ? (dec * a.q_scale) * qk[r] : 0.f;
-            if constexpr (GDN) gv[r] = (m && !((self >> r) & 1u)) ? (t.bi * dec) * kk[r] : 0.f;
-          }
+        for (int ks = 0; ks < KS; ++ks) {
+          kj[ks] = kfrag(kTile * J, ks);
+          if constexpr (GDN) kfi[ks] = kfrag(kTile * I, ks);
         }
-        if constexpr (GDN) {
-          if (J == I) {   // the in-tile block: row-major to LDS, zero in the operand
-            *reinterpret_cast<f32x4*>(gin + lr * kTile + 4 * lg) = f32x4{gv[0], gv[1], gv[2], gv[3]};
+        const uint64_t mw = (i < T) ? s_mask[i * W + (J >> 2)] : 0ull;   // M+ row of node i
+        const f32x4 clj = *reinterpret_cast<const f32x4*>(s_cl + kTile * J + 4 * lg);
+        f32x4 qk = f32x4{0.f, 0.f, 0.f, 0.f}, kk = qk;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) gv[r] = 0.f;
-          }
+        for (int ks = 0; ks < KS; ++ks) {
+          qk = mfma16(kj[ks], qf[ks], qk);               // rows j, column i: k_j . q_i
+          if constexpr (GDN) kk = mfma16(kj[ks], kfi[ks], kk);
         }
-        split2_bf16(cv[0], cv[1], cw[hf][0], cw[hf][2]);
-        split2_bf16(cv[2], cv[3], cw[hf][1], cw[hf][3]);
-        if constexpr (GDN) {   // stored negated: U^T (-G)^T is subtracted by accumulation
-          split2_bf16(-gv[0], -gv[1], gw[hf][0], gw[hf][2]);
-          split2_bf16(-gv[2], -gv[3], gw[hf][1], gw[hf][3]);
+        const unsigned mb = (unsigned)(mw >> ((J & 3) * kTile + 4 * lg)) & 0xFu;
+        const unsigned self = (J == I) ? (1u << lr) >> (4 * lg) : 0u;   // bit r: j == i
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool m = (mb >> r) & 1u;
+          const float dec = __builtin_amdgcn_exp2f(t.cli - clj[r]);
+          cv[r] = m ? (dec * a.q_scale) * qk[r] : 0.f;
+          if constexpr (GDN) gv[r] = (m && !((self >> r) & 1u)) ? (t.bi * dec) * kk[r] : 0.f;
         }
       }
-      unsigned char* pc = buf + ((c * NF) * 64 + lane) * 16;
-      *reinterpret_cast<uint4*>(pc) = uint4{cw[0][0], cw[0][1], cw[1][0], cw[1][1]};
-      *reinterpret_cast<uint4*>(pc + 1024) = uint4{cw[0][2], cw[0][3], cw[1][2], cw[1][3]};
       if constexpr (GDN) {
-        *reinterpret_cast<uint4*>(pc + 2048) = uint4{gw[0][0], gw[0][1], gw[1][0], gw[1][1]};
-        *reinterpret_cast<uint4*>(pc + 3072) = uint4{gw[0][2], gw[0][3], gw[1][2], gw[1][3]};
+        if (J == I) {   // the in-tile block: row-major to LDS, zero in the operand
+          *reinterpret_cast<f32x4*>(gin + lr * kTile + 4 * lg) = f32x4{gv[0], gv[1], gv[2], gv[3]};
+#pragma unroll
+          for (int r = 0; r < 4; ++r) gv[r] = 0.f;
+        }
+      }
+      // this half's 8 bytes of each 16-byte operand piece: hi01 hi23, then lo01 lo23
+      uint32_t cw[4], gw[4];
+      split2_bf16(cv[0], cv[1], cw[0], cw[2]);
+      split2_bf16(cv[2], cv[3], cw[1], cw[3]);
+      unsigned char* pc = buf + ((c * NF) * 64 + lane) * 16 + hf * 8;
+      *reinterpret_cast<uint2*>(pc) = uint2{cw[0], cw[1]};
+      *reinterpret_cast<uint2*>(pc + 1024) = uint2{cw[2], cw[3]};
+      if constexpr (GDN) {   // stored negated: U^T (-G)^T is subtracted by accumulation
+        split2_bf16(-gv[0], -gv[1], gw[0], gw[2]);
+        split2_bf16(-gv[2], -gv[3], gw[1], gw[3]);
+        *reinterpret_cast<uint2*>(pc + 2048) = uint2{gw[0], gw[1]};
+        *reinterpret_cast<uint2*>(pc + 3072) = uint2{gw[2], gw[3]};
       }
     }
   };
 
   // 2.-3. value rows of this wave for tile I: the delta-rule solve, then the
-  // readout; returns O^T (the store is left to the caller)
+  // readout; returns O^T (the store is left to the caller).  The chunks of
+  // earlier tiles hold final U^T columns, so their correction and readout
+  // terms run as interleaved MFMA chains, independent of the B0 products;
+  // only the chunk of tile I itself waits for the in-tile solve.
+  struct ChunkOps {
+    bf16x8 ch, cl, gh, gl, uh, ul;
+  };
   auto value_work = [&](int I, const bf16x8 (&qf)[KS], const bf16x4 vcur, const TileIn& t,
                         const unsigned char* buf, const float* gin) __attribute__((always_inline)) {
-    const int nc = I / 2 + 1;
+    const int cI = I / 2;   // the chunk that holds tile I
     const int i = kTile * I + lr;
     const bool iv = i < T;
-    auto chunk_live = [&](int c) __attribute__((always_inline)) {   // uniform: any ancestor of tile I in chunk c
-      return tile_bits32(I, c) != 0u;
-    };
     auto pc = [&](int c, int k) __attribute__((always_inline)) { return buf + ((c * NF + k) * 64 + lane) * 16; };
-    // B0^T = S Q_I^T (and S K_I^T for the delta rule)
+    auto load_ops = [&](int c, ChunkOps& o) __attribute__((always_inline)) {
+      o.ch = *reinterpret_cast<const bf16x8*>(pc(c, 0));
+      o.cl = *reinterpret_cast<const bf16x8*>(pc(c, 1));
+      o.uh = ufrag(s_ut, c);
+      if constexpr (GDN) {
+        o.gh = *reinterpret_cast<const bf16x8*>(pc(c, 2));
+        o.gl = *reinterpret_cast<const bf16x8*>(pc(c, 3));
+        o.ul = ufrag(s_utl, c);
+      }
+    };
+    // chunks with an ancestor of tile I (uniform)
+    uint32_t live = 0;
+#pragma unroll
+    for (int c = 0; c < 2 * W; ++c) live |= (tile_bits32(I, c) != 0u ? 1u : 0u) << c;
+    live = __builtin_amdgcn_readfirstlane(live);
+    f32x4 x = f32x4{0.f, 0.f, 0.f, 0.f}, acc = x, acc2 = x;
+    // B0^T = S Q_I^T (and S K_I^T for the delta rule), independent of the chunks
     f32x4 b0 = f32x4{0.f, 0.f, 0.f, 0.f}, sk = b0;
     bf16x8 kfi[KS];
     if constexpr (GDN) {
@@ -397,23 +414,36 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
         sk = mfma16(slo[ks], kfi[ks], sk);
       }
     }
+    // the chunks of earlier tiles (for gated linear attention: all of them)
+    for (int c = 0; c < (GDN ? cI : cI + 1); ++c) {
+      if (!((live >> c) & 1u)) continue;   // uniform
+      ChunkOps o;
+      load_ops(c, o);
+      if constexpr (GDN) {
+        x = mfma16(o.uh, o.gh, x);
+        acc = mfma16(o.uh, o.ch, acc);
+        x = mfma16(o.uh, o.gl, x);
+        acc2 = mfma16(o.uh, o.cl, acc2);
+        x = mfma16(o.ul, o.gh, x);
+        acc = mfma16(o.ul, o.ch, acc);
+      } else {
+        acc = mfma16(o.uh, o.ch, acc);
+        acc = mfma16(o.uh, o.cl, acc);
+      }
+    }
     const float Pi = iv ? __builtin_amdgcn_exp2f(t.cli) : 0.f;
 
     if constexpr (GDN) {
-      // 2. U_I: X = beta (V - P S K^T), plus U^T (-G)^T over earlier tiles ...
-      f32x4 x;
+      // 2. U_I: X = beta (V - P S K^T) - U^T G^T over the earlier tiles (in x),
+      // then the chunk of tile I: the G columns of tile I are zero there (its
+      // block is solved below) and those of tile I - 1 are final
+      ChunkOps o;
+      load_ops(cI, o);
+      x = mfma16(o.uh, o.gh, x);
+      x = mfma16(o.uh, o.gl, x);
+      x = mfma16(o.ul, o.gh, x);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) x[r] = t.bi * ((float)vcur[r] - Pi * sk[r]);
-      for (int c = 0; c < nc; ++c) {
-        if (!chunk_live(c)) continue;
-        const bf16x8 ghi = *reinterpret_cast<const bf16x8*>(pc(c, 2));
-        const bf16x8 glo = *reinterpret_cast<const bf16x8*>(pc(c, 3));
-        const bf16x8 uhi = ufrag(s_ut, c);
-        const bf16x8 ulo = ufrag(s_utl, c);
-        x = mfma16(uhi, ghi, x);
-        x = mfma16(uhi, glo, x);
-        x = mfma16(ulo, ghi, x);
-      }
+      for (int r = 0; r < 4; ++r) x[r] += t.bi * ((float)vcur[r] - Pi * sk[r]);
       // ... then the in-tile ancestors, in index order (lane (j, lg) holds u_j)
       unsigned tin = s_tin[I];
       while (tin) {   // uniform
@@ -436,19 +466,17 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
         s_ut[at] = __builtin_bit_cast(__bf16, (uint16_t)(ub >> 16));
         s_utl[at] = (__bf16)rem;
       }
+      // 3. the readout term of tile I's chunk, with U_I now in place (the
+      // wave's own rows: its LDS writes above are read back in order)
+      const bf16x8 uh = ufrag(s_ut, cI), ul = ufrag(s_utl, cI);
+      acc = mfma16(uh, o.ch, acc);
+      acc2 = mfma16(uh, o.cl, acc2);
+      acc = mfma16(ul, o.ch, acc);
     }
-
-    // 3. readout: O^T = q_scale P_i B0^T + U^T C^T (U = V for gated linear attention)
-    f32x4 acc = (Pi * a.q_scale) * b0;
-    for (int c = 0; c < nc; ++c) {
-      if (!chunk_live(c)) continue;
-      const bf16x8 chi = *reinterpret_cast<const bf16x8*>(pc(c, 0));
-      const bf16x8 clo = *reinterpret_cast<const bf16x8*>(pc(c, 1));
-      const bf16x8 uhi = ufrag(s_ut, c);
-      acc = mfma16(uhi, chi, acc);
-      acc = mfma16(uhi, clo, acc);
-      if constexpr (GDN) acc = mfma16(ufrag(s_utl, c), chi, acc);
-    }
+    // 3. O^T = q_scale P_i B0^T + U^T C^T (U = V for gated linear attention)
+    const float ps = Pi * a.q_scale;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r] = ps * b0[r] + (acc[r] + acc2[r]);
     return acc;
   };
 
