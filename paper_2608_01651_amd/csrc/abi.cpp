@@ -249,6 +249,9 @@ tl_status tree_conv_gates(const tl_problem* problem, int32_t conv_width, float n
   a.num_slots = problem->num_slots;
   a.tiles = 0;
   a.eps = norm_eps;
+#ifdef TL_TRACE
+  a.trace = g_trace;
+#endif
   return tl::launch_conv_gates(a, conv_width, gdn, reinterpret_cast<hipStream_t>(stream));
 }
 

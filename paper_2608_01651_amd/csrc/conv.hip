@@ -59,6 +59,7 @@ __global__ __launch_bounds__(kThreads) void conv_gates_kernel(ConvArgs a) {
   const int tile = blockIdx.x % a.tiles, b = blockIdx.x / a.tiles;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int C = a.C;
+  TL_TRACE_POINT(a, 0);
   const int c0 = tile * CT + (lane % LPN) * 8;
   const bool live = c0 < C;
   const int cc = live ? c0 : C - 8;   // dead lanes read a valid chunk and store nothing
@@ -113,6 +114,7 @@ __global__ __launch_bounds__(kThreads) void conv_gates_kernel(ConvArgs a) {
   const float alog = a.A_log[gh], dtb = a.dt_bias[gh];
   if (tid < T) s_par[tid] = par;
   wait_vmem();   // the direct copies (and everything else requested above)
+  TL_TRACE_POINT(a, 1);
   if (__syncthreads_or(tid < T && !(par == -1 || (par >= 0 && par < tid)))) {
     if (tid == 0) report(a.dev_err, TL_EBADTREE);
     return;
@@ -144,6 +146,7 @@ __global__ __launch_bounds__(kThreads) void conv_gates_kernel(ConvArgs a) {
     dst_row = (size_t)a.Hv * a.dv;
   }
   const int lo = (lane % LPN) * 16;   // the lane's byte offset in a tile row
+  TL_TRACE_POINT(a, 2);
 
   for (int base = 0; base < T; base += kWaves * NPW) {
     const int n = base + wave * NPW + lane / LPN;
@@ -193,6 +196,7 @@ __global__ __launch_bounds__(kThreads) void conv_gates_kernel(ConvArgs a) {
       *reinterpret_cast<bf16x8*>(dst0 + (size_t)(rq.off + n) * dst_row) = out;
     }
   }
+  TL_TRACE_POINT(a, 3);
 }
 
 // Channel tile of conv_gates.  Wider tiles (256, 512 channels: more bytes

@@ -117,6 +117,9 @@ struct ConvArgs {
   int batch, Hk, Hv, dk, dv, C, max_nodes, num_slots;
   int tiles;   // channel tiles per request (set by the launcher)
   float eps;
+#ifdef TL_TRACE
+  long long* trace;  // [blocks][16] wall-clock stamps (trace builds only)
+#endif
 };
 
 // tree_conv_state_commit
