@@ -147,7 +147,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     const int p = base + lane;
     if (p < T * CPRK) {
       const int r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
-      copy16_to_lds(Kb + (size_t)r * qk_row + c * 8, s_k + (size_t)base * 8);
+      copy16_to_lds_async(Kb + (size_t)r * qk_row + c * 8, s_k + (size_t)base * 8);
     }
   }
   const int npair = (T + 1) >> 1;
