@@ -576,9 +576,9 @@ def main():
                     help="only time a plain 512 MiB device copy (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(every (request, head) unit is independent; see the design notes on sharding).",
-              file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(every (request, head) unit is independent, so the path shards over requests "
+              "or head groups without communication).", file=sys.stderr)
         sys.exit(2)
 
     def log(msg):

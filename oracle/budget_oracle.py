@@ -20,7 +20,7 @@ What is computed
   into the flat forest: node_offsets, parents in packed numbering, and the
   candidate row of every packed node.
 
-Readings (the paper leaves these open; the design notes list them)
+Readings (the paper leaves these open; the kernels take the same ones)
 -------------------------------------------------------------------
 * rho is formed in fp32, root first, one rounding per step:
   rho(root) = p(root), rho(v) = fl32(rho(parent) * p(v)).  Its bits decide

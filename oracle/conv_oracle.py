@@ -21,7 +21,7 @@ What is computed, and where the paper defines it
 * The commit keeps, as the new convolution state, the last width-1 inputs of
   the sequence prefix + accepted path (the accepted path of §4.4).
 
-Readings (the paper fixes none of these formulas; the design notes list them)
+Readings (the paper fixes none of these formulas; the kernels take the same ones)
 ------------------------------------------------------------------------------
 * x[r] is the node's mixed projection row [q | k | v] of
   C = 2 Hk d_k + Hv d_v channels.  Channel c of node i:

@@ -21,7 +21,7 @@ What is computed, and where the paper defines it
   Eq. accepted-commit in §4.4), i.e. the same walk over the accepted path; an
   empty path leaves S_pre unchanged (end of §4.4).
 
-Conventions (readings of the paper; each is also listed in the design notes)
+Conventions (readings of the paper; the kernels take the same ones)
 ------------------------------------------------------------------------------
 * Stored state orientation: the paper's state is S in R^{d_k x d_v} with
   o = S^T q; slots use the canonical [H, d_v, d_k] layout (§4.4).  The oracle
