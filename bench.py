@@ -371,11 +371,12 @@ def budget_leg(args, log):
     src = torch.empty(case.capacity, **i32)
     err = torch.zeros(1, **i32)
     prob_t = tl.problem(B, 1, 1, 16, 16, case.max_nodes)
+    ws = tl.budget_workspace(B, case.max_nodes, device=dev)
     log(f"budget allocation: {args.workload} B={B} candidates={M} capacity={case.capacity} "
         f"max_nodes={case.max_nodes}")
 
     def run():
-        tl.budget_select(prob_t, M, case.capacity, t_offs, t_par, t_prob, rho, rank, no, fpar, src,
+        tl.budget_select(prob_t, M, case.capacity, t_offs, t_par, t_prob, rho, rank, no, fpar, src, ws,
                          dev_err=err)
 
     for _ in range(max(1, args.warmup)):
@@ -415,7 +416,7 @@ def budget_leg(args, log):
         "config": {"workload": f"{args.workload} candidate batch: B={B}, {M} candidates, "
                                f"capacity {case.capacity}, max_nodes {case.max_nodes}",
                    "selected": N},
-        "roofline": {"bound": "latency", "kernel": "tree_budget_select (3 launches)",
+        "roofline": {"bound": "latency", "kernel": "tree_budget_select (2 launches)",
                      "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 5), "algorithmic_bytes": int(nbytes)},
     }

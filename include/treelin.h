@@ -254,22 +254,29 @@ tl_status tree_conv_state_commit(const tl_problem* problem, int32_t conv_width,
  *   request-local, cand_prob [num_candidates] fp32; rho, rank
  *   [num_candidates]; parent, src [capacity].  Only batch and max_nodes of
  *   `problem` are used (the rest is checked as for tree_lin_attn_verify).
+ * workspace: caller-owned device memory of at least
+ *   tree_budget_workspace_bytes(B, max_nodes) bytes, 256-byte aligned; its
+ *   contents need no initialisation and are overwritten (calls that share a
+ *   workspace must not overlap).
  * Bounds: B <= 1024, M_b <= 1024, num_candidates <= 32768 (TL_EUNSUPPORTED
  *   on the host; a device size beyond them is TL_EINVAL).
  * Device errors: TL_EBADTREE (offsets), TL_EINVAL (a request with more than
  *   1024 candidates or more roots than max_nodes, capacity below the roots):
  *   nothing is selected and node_offsets is all zero.  Per request,
  *   TL_EBADTREE (a bad parent) or TL_EINVAL (a probability outside [0, 1]):
- *   that request keeps only its roots, its rho and rank are unspecified.
- * node_offsets[1..B] also carries a count between the launches, so it must
- * not alias the candidate arrays. */
+ *   that request keeps only its roots, its rho and rank are unspecified. */
 tl_status tree_budget_select(const tl_problem* problem, int32_t num_candidates, int32_t capacity,
                              const int32_t* cand_offsets, const int32_t* cand_parent,
                              const float* cand_prob,
                              float* rho, int32_t* rank,     /* [num_candidates] out */
                              int32_t* node_offsets,         /* [B+1] out */
                              int32_t* parent, int32_t* src, /* [capacity] out */
+                             void* workspace, size_t workspace_bytes,
                              int32_t* dev_err, void* stream);
+
+/* Bytes of tree_budget_select's workspace for a batch of `batch` requests
+ * and a per-request bound of `max_nodes` nodes (0 for an empty batch). */
+size_t tree_budget_workspace_bytes(int32_t batch, int32_t max_nodes);
 
 /* Tree topology of §4.1's notation table, as the kernels build it:
  * anc_mask[r, w] (W = ceil(max_nodes/64) uint64 words per node) has bit

@@ -285,10 +285,16 @@ tl_status tree_conv_state_commit(const tl_problem* problem, int32_t conv_width,
   return tl::launch_conv_state_commit(a, conv_width, reinterpret_cast<hipStream_t>(stream));
 }
 
+size_t tree_budget_workspace_bytes(int32_t batch, int32_t max_nodes) {
+  if (batch <= 0 || max_nodes <= 0) return 0;
+  return tl::budget_workspace_layout(batch, max_nodes).total;
+}
+
 tl_status tree_budget_select(const tl_problem* problem, int32_t num_candidates, int32_t capacity,
                              const int32_t* cand_offsets, const int32_t* cand_parent,
                              const float* cand_prob, float* rho, int32_t* rank,
                              int32_t* node_offsets, int32_t* parent, int32_t* src,
+                             void* workspace, size_t workspace_bytes,
                              int32_t* dev_err, void* stream) {
   tl_status st = check_problem(problem);
   if (st != TL_OK) return st;
@@ -297,13 +303,16 @@ tl_status tree_budget_select(const tl_problem* problem, int32_t num_candidates, 
   if (problem->batch > tl::kBudgetMaxBatch || num_candidates > tl::kBudgetMaxCandidates)
     return TL_EUNSUPPORTED;
   if (!cand_offsets || !cand_parent || !cand_prob || !rho || !rank || !node_offsets || !parent ||
-      !src)
+      !src || !workspace)
     return TL_EINVAL;
   if (!aligned(cand_offsets, 4) || !aligned(cand_parent, 4) || !aligned(cand_prob, 4) ||
       !aligned(rho, 4) || !aligned(rank, 4) || !aligned(node_offsets, 4) || !aligned(parent, 4) ||
-      !aligned(src, 4))
+      !aligned(src, 4) || !aligned(workspace, 256))
     return TL_EINVAL;
   if (dev_err && !aligned(dev_err, 4)) return TL_EINVAL;
+  const tl::BudgetWorkspace W = tl::budget_workspace_layout(problem->batch, problem->max_nodes);
+  if (workspace_bytes < W.total) return TL_EINVAL;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
   tl::BudgetArgs a;
   a.cand_offsets = cand_offsets;
   a.cand_parent = cand_parent;
@@ -314,6 +323,10 @@ tl_status tree_budget_select(const tl_problem* problem, int32_t num_candidates, 
   a.parent = parent;
   a.src = src;
   a.dev_err = dev_err;
+  a.ws_meta = reinterpret_cast<int32_t*>(ws + W.meta);
+  a.ws_key = reinterpret_cast<uint32_t*>(ws + W.key);
+  a.ws_cand = reinterpret_cast<uint32_t*>(ws + W.cand);
+  a.ws_root = reinterpret_cast<uint16_t*>(ws + W.root);
   a.batch = problem->batch;
   a.max_nodes = problem->max_nodes;
   a.num_candidates = num_candidates;

@@ -13,19 +13,18 @@
 // order, into the flat forest that verification takes.
 //
 // Two launches of fixed shape (a round can be captured once and replayed):
-//  1. rho_rank_kernel, one workgroup of 1024 per request, one candidate per
-//     thread: rho in fp32, root first, one rounding per step (Jacobi sweeps
-//     in LDS: after k sweeps every node of depth < k holds its final value),
-//     then each non-root candidate's rank in its request's order: the number
-//     of (rho, index) keys above its own, read by broadcast from LDS.  The
-//     request's root count (negated minus one when the request is rejected)
-//     goes to node_offsets[b + 1] for the second launch.
+//  1. rho_rank_kernel, up to 16 workgroups of 1024 per request (about 512
+//     in all), one candidate per thread: rho in fp32, root first, one
+//     rounding per step (Jacobi sweeps in LDS: after k sweeps every node of
+//     depth < k holds its final value), then each non-root candidate's rank
+//     in its request's order: the number of (rho, index) keys above its own,
+//     read by broadcast from LDS.  Each workgroup ranks one band of the
+//     request's candidates, its waves splitting the keys.  The request's
+//     eligible candidates (ranks below e_b = min(max_nodes, M_b) - roots) go
+//     to the workspace in rank order, as rho bits and local indices with
+//     their parents, next to its roots and its counts.
 //  2. select_pack_kernel, one workgroup of 1024:
-//     - a request's eligible candidates are its ranks below
-//       e_b = min(max_nodes, M_b) - roots, so the eligible total E and every
-//       request's place in a sorted key array follow from the offsets alone;
-//     - one coalesced sweep scatters each eligible candidate's rho bits to
-//       position base_b + rank: per request a descending list in LDS;
+//     - the eligible lists, each already sorted, are copied to LDS;
 //     - a radix selection (11, 11 and 9 bits) finds the rho t of the K-th best
 //       eligible candidate (K = the capacity left after the roots) and how
 //       many candidates with rho exactly t are still to be taken; on sorted
@@ -35,12 +34,14 @@
 //       the ties go to the lowest batch-wide indices, i.e. to requests in
 //       batch order; budget = roots + taken, and a scan gives node_offsets;
 //     - packing: the selected nodes are the roots and the `budget - roots`
-//       best-ranked candidates (always such a prefix of the request's order);
-//       in batch order, a node's packed row is the number of selected
-//       candidates before it, so coalesced sweeps over contiguous per-wave
-//       segments, ballots and one scan of the wave totals number them, and
-//       parents are renumbered through LDS.
+//       first entries of the request's list (always a prefix-connected set);
+//       each sets its bit in a bitmap over the batch's candidates, and in
+//       batch order a node's packed row is the number of set bits before it
+//       (a scan over the bitmap's words); parents are renumbered the same way.
+//     Only the eligible and the selected candidates are touched here.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 
 #include "tl_device.h"
 #include "tl_kernels.h"
@@ -51,12 +52,11 @@ namespace {
 
 constexpr int kRankThreads = kBudgetMaxTree;          // launch 1: one candidate per thread
 constexpr int kRankWaves = kRankThreads / 64;
+constexpr int kRankBlocks = 512;                        // launch 1: target workgroups
 constexpr int kSelWaves = kSelectThreads / 64;
 constexpr int kBins = 2048;                            // widest radix digit: 11 bits
-constexpr int kSegChunks = kBudgetMaxCandidates / (kSelWaves * 64);   // 64-candidate chunks per wave
 constexpr int kNotEligible = 0x7fffffff;              // rank of a rejected request's non-roots
 
-static_assert(kSegChunks <= 32, "a wave's selection bits must fit one 32-bit mask");
 
 // A request's candidate range is usable when it lies inside the arrays and
 // fits the per-request bound; the second launch rejects the batch otherwise.
@@ -65,12 +65,6 @@ __device__ inline bool range_ok(int o0, int o1, int num_candidates) {
 }
 
 __device__ inline int lane_id() { return (int)(threadIdx.x & 63); }
-
-// lanes below this one whose bit is set in `mask`
-__device__ inline int lanes_below(uint64_t mask) {
-  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                        __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-}
 
 __device__ inline int wave_sum(int x) {
 #pragma unroll
@@ -126,23 +120,6 @@ __device__ inline uint64_t order_key(float rho, int v) {
   return ((uint64_t)(__float_as_uint(rho) & 0x7fffffffu) << 32) | (uint64_t)(0xffffffffu - (uint32_t)v);
 }
 
-// The request of candidate i: the last b with s_offs[b] <= i (i < s_offs[B]).
-__device__ inline int request_of(const int* s_offs, int B, int i) {
-  int lo = 0, hi = B - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (s_offs[mid] <= i) lo = mid;
-    else hi = mid - 1;
-  }
-  return lo;
-}
-
-// Moves b forward to the request that holds candidate i (i increases).
-__device__ inline int advance_request(const int* s_offs, int B, int b, int i) {
-  while (b < B - 1 && s_offs[b + 1] <= i) ++b;
-  return b;
-}
-
 // Number of leading keys of the descending list L[0..n) that are > t
 // (STRICT false) or >= t (STRICT true).
 template <bool STRICT>
@@ -161,14 +138,27 @@ __device__ inline int count_above(const uint32_t* L, int n, uint32_t t) {
 // ---------------------------------------------------------------------------
 // 1. rho and ranks
 // ---------------------------------------------------------------------------
+// Launch 1 runs `slices` workgroups per request (block = request * slices +
+// slice).  Every one of them loads the whole tree and computes every rho (the
+// sweep needs all of them), then ranks only its own band of candidates, with
+// the 16 waves splitting the keys of the request between them; slice 0 also
+// writes the request's roots and meta entries.
 __global__ __launch_bounds__(kRankThreads) void rho_rank_kernel(BudgetArgs a) {
   __shared__ float s_rho[2][kBudgetMaxTree];
   __shared__ __align__(16) uint64_t s_key[kBudgetMaxTree + 8];
+  __shared__ int s_cnt[kBudgetMaxTree];
   __shared__ int s_part[kRankWaves];
-  const int b = blockIdx.x, v = threadIdx.x;
+  const int slices = (int)gridDim.x / a.batch;
+  const int b = (int)blockIdx.x / slices, s = (int)blockIdx.x - b * slices, v = threadIdx.x;
+  const int lane = v & 63, wave = v >> 6;
   const int o0 = a.cand_offsets[b], o1 = a.cand_offsets[b + 1];
   if (!range_ok(o0, o1, a.num_candidates)) return;   // the second launch reports it
   const int M = o1 - o0;
+  // this slice's band [c0, c1): bands of a multiple of 64 candidates
+  const int C = max(64, ((M + slices - 1) / slices + 63) & ~63);
+  const int c0 = s * C, c1 = min(M, c0 + C);
+  if (s > 0 && c0 >= c1) return;   // an empty band (slice 0 always runs)
+  const bool mine_band = v >= c0 && v < c1;
   TL_TRACE_POINT(a, 0);
   int p = -2, tree_bad = 0, prob_bad = 0;
   float pr = 0.f;
@@ -179,14 +169,28 @@ __global__ __launch_bounds__(kRankThreads) void rho_rank_kernel(BudgetArgs a) {
     tree_bad = !(p == -1 || (p >= 0 && p < v));
     prob_bad = !(pr >= 0.f && pr <= 1.f);   // NaN fails too
   }
-  const int roots = block_sum<kRankWaves>(p == -1, s_part);
+  const int mn = a.max_nodes;
+  int roots;
+  if (s == 0) {   // roots: their count, and their indices in order into the workspace
+    const int rix = block_inclusive_scan<kRankWaves>(p == -1, s_part, &roots) - (p == -1);
+    if (p == -1 && rix < mn) a.ws_root[(size_t)b * mn + rix] = (uint16_t)v;
+  } else {
+    roots = __syncthreads_count(p == -1);
+  }
   const bool any_tree_bad = __syncthreads_or(tree_bad), any_prob_bad = __syncthreads_or(prob_bad);
   TL_TRACE_POINT(a, 1);
-  if (v == 0) a.node_offsets[b + 1] = (any_tree_bad || any_prob_bad) ? -(roots + 1) : roots;
-  if (any_tree_bad || any_prob_bad) {
+  const bool rejected = any_tree_bad || any_prob_bad;
+  // eligible candidates: ranks below min(max_nodes, M) - roots (none if rejected)
+  const int elig = rejected ? 0 : max(0, min(mn, M) - roots);
+  if (s == 0 && v == 0) {
+    a.ws_meta[4 * b] = roots;
+    a.ws_meta[4 * b + 1] = elig;
+    a.ws_meta[4 * b + 2] = rejected;
+  }
+  if (rejected) {
     // the request keeps its roots and nothing else
-    if (v == 0) report(a.dev_err, any_tree_bad ? TL_EBADTREE : TL_EINVAL);
-    if (v < M) {
+    if (s == 0 && v == 0) report(a.dev_err, any_tree_bad ? TL_EBADTREE : TL_EINVAL);
+    if (mine_band) {
       a.rho[o0 + v] = 0.f;
       a.rank[o0 + v] = p == -1 ? -1 : kNotEligible;
     }
@@ -206,27 +210,49 @@ __global__ __launch_bounds__(kRankThreads) void rho_rank_kernel(BudgetArgs a) {
   }
   TL_TRACE_POINT(a, 2);
   const float rho = v < M ? s_rho[cur][v] : 0.f;
-  const uint64_t mine = v < M && p >= 0 ? order_key(rho, v) : 0ull;
-  s_key[v] = mine;   // zero for roots and past M
+  s_key[v] = v < M && p >= 0 ? order_key(rho, v) : 0ull;   // zero for roots and past M
   if (v < 8) s_key[kBudgetMaxTree + v] = 0ull;
+  if (v < C) s_cnt[v] = 0;
   __syncthreads();
-  if (v < M) {
-    // rank = keys above mine (roots and padding have key 0: never above)
-    int cnt = 0;
+  // rank = keys above mine (roots and padding have key 0: never above).
+  // Work items: (64-candidate block of the band, part of the key range)
+  {
+    const int nblk = (c1 - c0 + 63) >> 6;          // 1 .. 16
+    const int parts = max(1, kRankWaves / nblk);
     const int M8 = (M + 7) & ~7;
-    for (int u = 0; u < M8; u += 8) {
-      uint64_t k[8];
+    const int span = ((M8 / 8 + parts - 1) / parts) * 8;
+    for (int it = wave; it < nblk * parts; it += kRankWaves) {   // uniform per wave
+      const int blk = it % nblk, part = it / nblk;
+      const int c = c0 + 64 * blk + lane;
+      const uint64_t mine = c < c1 ? s_key[c] : ~0ull;   // past the band: counts nothing
+      const int u0 = part * span, u1 = min(M8, u0 + span);
+      int cnt = 0;
+      for (int u = u0; u < u1; u += 8) {
+        uint64_t k[8];
 #pragma unroll
-      for (int j = 0; j < 8; j += 2) {
-        const ulonglong2 two = *reinterpret_cast<const ulonglong2*>(&s_key[u + j]);
-        k[j] = two.x;
-        k[j + 1] = two.y;
+        for (int j = 0; j < 8; j += 2) {
+          const ulonglong2 two = *reinterpret_cast<const ulonglong2*>(&s_key[u + j]);
+          k[j] = two.x;
+          k[j + 1] = two.y;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) cnt += k[j] > mine;
       }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) cnt += k[j] > mine;
+      if (c < c1) {
+        if (parts == 1) s_cnt[c - c0] = cnt;
+        else atomicAdd(&s_cnt[c - c0], cnt);
+      }
     }
+  }
+  __syncthreads();
+  if (mine_band) {
+    const int cnt = s_cnt[v - c0];
     a.rho[o0 + v] = rho;
     a.rank[o0 + v] = p < 0 ? -1 : cnt;
+    if (p >= 0 && cnt < elig) {   // the request's eligible list, in rank order
+      a.ws_key[(size_t)b * mn + cnt] = __float_as_uint(rho) & 0x7fffffffu;
+      a.ws_cand[(size_t)b * mn + cnt] = (uint32_t)v | (uint32_t)(p + 1) << 16;
+    }
   }
   TL_TRACE_POINT(a, 3);
 }
@@ -234,29 +260,19 @@ __global__ __launch_bounds__(kRankThreads) void rho_rank_kernel(BudgetArgs a) {
 // ---------------------------------------------------------------------------
 // 2. batch-wide selection, budgets, node_offsets and packing
 // ---------------------------------------------------------------------------
+// LDS of select_pack_kernel: the histogram, five per-request arrays, and a
+// region that holds the sorted key lists during the selection and the
+// candidates' selection bitmap with its word offsets during the packing.
+__host__ __device__ inline int budget_region_words(int num_candidates) {
+  const int words = (num_candidates + 31) / 32;
+  return num_candidates > 2 * words ? num_candidates : 2 * words;
+}
+
 int budget_select_lds_bytes(int batch, int num_candidates) {
-  return 4 * (kBins + (batch + 1) + 4 * batch + num_candidates);
+  return 4 * (kBins + (batch + 1) + 4 * batch + budget_region_words(num_candidates));
 }
 
 namespace {
-
-// A lane's request while it walks its candidates in increasing order.
-struct Cursor {
-  int b, end;   // request b holds candidates up to end - 1
-  __device__ void seek(const int* s_offs, int B, int i) {
-    b = request_of(s_offs, B, i);
-    end = s_offs[b + 1];
-  }
-  // Moves to the request of candidate i (i never decreases); true if it changed.
-  __device__ bool advance(const int* s_offs, int B, int i) {
-    if (i < end) return false;
-    do {
-      ++b;
-      end = s_offs[b + 1];
-    } while (b < B - 1 && end <= i);
-    return true;
-  }
-};
 
 // Wave 0, after a histogram pass: the bin that holds the krem-th largest
 // active key (lane l owns bins l*PER .. l*PER+PER-1, read and cleared as int4).
@@ -325,21 +341,27 @@ __global__ __launch_bounds__(kSelectThreads) void select_pack_kernel(BudgetArgs 
   extern __shared__ __align__(16) int s_dyn[];
   __shared__ int s_part[kSelWaves];
   __shared__ int s_flag, s_prefix, s_krem;
-  const int B = a.batch, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int B = a.batch, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, mn = a.max_nodes;
+  constexpr int kGroup = 8;   // requests per wave whose lists are in flight together
   int* s_hist = s_dyn;               // [kBins] (16-byte aligned: read as int4)
   int* s_offs = s_hist + kBins;      // [B + 1] candidate offsets
   int* s_roots = s_offs + B + 1;     // [B] roots
   int* s_elig = s_roots + B;         // [B] eligible candidates e_b, then taken ones
-  int* s_base = s_elig + B;          // [B] start of the request's sorted list
+  int* s_base = s_elig + B;          // [B] start of the request's sorted list in s_key
   int* s_noff = s_base + B;          // [B] packed offset of the request
-  uint32_t* s_key = reinterpret_cast<uint32_t*>(s_noff + B);   // [num_candidates] sorted lists
-  int* s_row = reinterpret_cast<int*>(s_key);                   // the same words: packed rows
+  uint32_t* s_key = reinterpret_cast<uint32_t*>(s_noff + B);        // the sorted lists, then ...
+  uint32_t* s_bits = s_key;                                          // ... a bit per candidate
+  int* s_wpre = reinterpret_cast<int*>(s_key) + (a.num_candidates + 31) / 32;   // and word offsets
   TL_TRACE_POINT(a, 8);
 
-  // -- shape, roots, eligible counts --------------------------------------
+  // -- shape, roots, eligible counts (from the first launch) ---------------
   if (tid == 0) s_flag = 0;
   for (int b = tid; b <= B; b += kSelectThreads) s_offs[b] = a.cand_offsets[b];
-  const int r_in = tid < B ? a.node_offsets[tid + 1] : 0;   // from launch 1
+  int r_in = 0, e_in = 0;
+  if (tid < B) {
+    r_in = a.ws_meta[4 * tid];
+    e_in = a.ws_meta[4 * tid + 1];
+  }
   for (int i = tid; i < kBins; i += kSelectThreads) s_hist[i] = 0;
   __syncthreads();
   int flags = 0, roots = 0, elig = 0;
@@ -349,11 +371,10 @@ __global__ __launch_bounds__(kSelectThreads) void select_pack_kernel(BudgetArgs 
   }
   if (tid < B) {
     const int m = s_offs[tid + 1] - s_offs[tid];
-    roots = r_in < 0 ? -r_in - 1 : r_in;
     flags |= m < 0;
-    flags |= (m > kBudgetMaxTree || roots > a.max_nodes) << 1;
-    // eligible: ranks below min(max_nodes - roots, non-roots); none if rejected
-    elig = r_in < 0 ? 0 : max(0, min(a.max_nodes, m) - roots);
+    flags |= (m > kBudgetMaxTree || r_in > mn) << 1;
+    roots = r_in;
+    elig = e_in;
     s_roots[tid] = roots;
     s_elig[tid] = elig;
   }
@@ -371,40 +392,32 @@ __global__ __launch_bounds__(kSelectThreads) void select_pack_kernel(BudgetArgs 
   const int ebase = block_inclusive_scan<kSelWaves>(elig, s_part, &E) - elig;
   if (tid < B) s_base[tid] = ebase;
   const int M = s_offs[B];
-  // contiguous per-wave candidate segments, whole chunks of 64
-  const int seg_len = (((M + kSelWaves - 1) / kSelWaves) + 63) & ~63;
-  const int seg0 = wave * seg_len, seg1 = min(seg0 + seg_len, M);
-  const int last = max(M - 1, 0);   // loads past the segment read this (in range) and are dropped
-  // every rank of the segment, all loads in flight at once (kept for the packing)
-  int r[kSegChunks];
-  Cursor cur0 = {B - 1, M};
-  if (M > 0) {
-#pragma unroll
-    for (int c = 0; c < kSegChunks; ++c) r[c] = a.rank[min(seg0 + 64 * c + lane, last)];
-    cur0.seek(s_offs, B, min(seg0 + lane, last));
-  }
   __syncthreads();   // s_base
   TL_TRACE_POINT(a, 9);
 
   int take = 0;   // this thread's request (tid < B): candidates taken
   if (K > 0 && K < E) {
-    // -- eligible keys into per-request descending lists --------------------
-    Cursor cu = cur0;
-    int eb = s_elig[cu.b], bb = s_base[cu.b];
+    // -- the eligible lists, already sorted, into LDS.  A list has at most
+    // max_nodes <= 256 keys, four 64-lane chunks: a wave loads eight requests'
+    // lists at once, then stores them
+    for (int b0 = wave; b0 < B; b0 += kGroup * kSelWaves) {   // uniform per wave
+      uint32_t t[kGroup][4];
 #pragma unroll
-    for (int h = 0; h < kSegChunks; h += kSegChunks / 2) {   // half a segment of rho loads at a time
-      float x[kSegChunks / 2];
+      for (int g = 0; g < kGroup; ++g) {
+        const int b = b0 + g * kSelWaves, n = b < B ? s_elig[b] : 0;
 #pragma unroll
-      for (int c = 0; c < kSegChunks / 2; ++c) x[c] = a.rho[min(seg0 + 64 * (h + c) + lane, last)];
+        for (int c = 0; c < 4; ++c) {
+          const int r = lane + 64 * c;
+          if (r < n) t[g][c] = a.ws_key[(size_t)b * mn + r];
+        }
+      }
 #pragma unroll
-      for (int c = 0; c < kSegChunks / 2; ++c) {
-        const int i = seg0 + 64 * (h + c) + lane;
-        if (i < seg1) {
-          if (cu.advance(s_offs, B, i)) {
-            eb = s_elig[cu.b];
-            bb = s_base[cu.b];
-          }
-          if (r[h + c] >= 0 && r[h + c] < eb) s_key[bb + r[h + c]] = __float_as_uint(x[c]) & 0x7fffffffu;
+      for (int g = 0; g < kGroup; ++g) {
+        const int b = b0 + g * kSelWaves, n = b < B ? s_elig[b] : 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int r = lane + 64 * c;
+          if (r < n) s_key[s_base[b] + r] = t[g][c];
         }
       }
     }
@@ -456,72 +469,84 @@ __global__ __launch_bounds__(kSelectThreads) void select_pack_kernel(BudgetArgs 
     s_elig[tid] = take;
   }
   if (tid == 0) a.node_offsets[0] = 0;
+  const int words = (M + 31) / 32;
+  for (int w = tid; w < words; w += kSelectThreads) s_bits[w] = 0u;   // the keys are dead
   __syncthreads();
   TL_TRACE_POINT(a, 12);
 
-  // -- packing: the row of a selected node = selected candidates before it --
-  // (roots have rank -1, a rejected request's other candidates never rank below its take)
-  uint32_t selbits = 0;
-  int count = 0;
-  {
-    Cursor cu = cur0;
-    int tk = s_elig[cu.b];
+  // -- packing: a bit per selected candidate (the roots and the best-ranked
+  // `take`, at most max_nodes <= 256 per request: four chunks of a wave); in
+  // batch order a node's packed row is the number of selected candidates
+  // before it, which a word scan of the bitmap gives.  A selected node's
+  // entry is its index in the request with its parent + 1 above bit 16 (0 for
+  // a root); up to kGroup * 16 requests the entries stay in registers between
+  // the two passes
+  using Entries = uint32_t[kGroup][4];
+  auto load_entries = [&](int b0, Entries& e) __attribute__((always_inline)) {
 #pragma unroll
-    for (int c = 0; c < kSegChunks; ++c) {
-      const int i = seg0 + 64 * c + lane;
-      if (i < seg1) {
-        if (cu.advance(s_offs, B, i)) tk = s_elig[cu.b];
-        const bool sel = r[c] == -1 || (r[c] >= 0 && r[c] < tk);
-        selbits |= (uint32_t)sel << c;
-        count += sel;
+    for (int g = 0; g < kGroup; ++g) {
+      const int b = b0 + g * kSelWaves;
+      const int nr = b < B ? s_roots[b] : 0, n = b < B ? nr + s_elig[b] : 0;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int j = lane + 64 * c;
+        if (j < n) e[g][c] = j < nr ? (uint32_t)a.ws_root[(size_t)b * mn + j] : a.ws_cand[(size_t)b * mn + (j - nr)];
       }
     }
-  }
-  const int wave_count = wave_sum(count);
-  int all_sel;
-  const int wave_incl = block_inclusive_scan<kSelWaves>(lane == 0 ? wave_count : 0, s_part, &all_sel);
-  int row = __shfl(wave_incl, 0, 64) - wave_count;   // rows before this wave's segment
+  };
+  auto apply = [&](int b0, const Entries& e, auto&& fn) __attribute__((always_inline)) {
 #pragma unroll
-  for (int c = 0; c < kSegChunks; ++c) {
-    const int i = seg0 + 64 * c + lane;
-    const bool sel = (selbits >> c) & 1u;
-    const uint64_t m = __ballot(sel);
-    if (i < seg1) s_row[i] = sel ? row + lanes_below(m) : -1;
-    row += __popcll(m);
-  }
-  TL_TRACE_POINT(a, 13);
-  int p[kSegChunks];
-  if (M > 0) {
+    for (int g = 0; g < kGroup; ++g) {
+      const int b = b0 + g * kSelWaves;
+      const int n = b < B ? s_roots[b] + s_elig[b] : 0;
 #pragma unroll
-    for (int c = 0; c < kSegChunks; ++c) {   // parents of the selected nodes only
-      const int i = seg0 + 64 * c + lane;
-      p[c] = a.cand_parent[((selbits >> c) & 1u) ? i : last];
+      for (int c = 0; c < 4; ++c)
+        if (lane + 64 * c < n) fn(b, s_offs[b], s_offs[b] + (int)(e[g][c] & 0xffffu), (int)(e[g][c] >> 16) - 1);
+    }
+  };
+  const bool resident = B <= kGroup * kSelWaves;
+  Entries kept;
+  if (resident) load_entries(wave, kept);
+  auto each_selected = [&](auto&& fn) __attribute__((always_inline)) {
+    if (resident) {
+      apply(wave, kept, fn);
+    } else {
+      for (int b0 = wave; b0 < B; b0 += kGroup * kSelWaves) {   // uniform per wave
+        Entries e;
+        load_entries(b0, e);
+        apply(b0, e, fn);
+      }
+    }
+  };
+  each_selected([&](int, int, int i, int) { atomicOr(&s_bits[i >> 5], 1u << (i & 31)); });
+  __syncthreads();
+  {
+    // word offsets: thread t scans words t * per .. t * per + per - 1
+    const int per = (words + kSelectThreads - 1) / kSelectThreads;
+    int cnt = 0;
+    for (int w = tid * per; w < min(words, (tid + 1) * per); ++w) cnt += __popc(s_bits[w]);
+    int all;
+    int run = block_inclusive_scan<kSelWaves>(cnt, s_part, &all) - cnt;
+    for (int w = tid * per; w < min(words, (tid + 1) * per); ++w) {
+      s_wpre[w] = run;
+      run += __popc(s_bits[w]);
     }
   }
   __syncthreads();
-  TL_TRACE_POINT(a, 14);
+  TL_TRACE_POINT(a, 13);
+  auto row_of = [&](int i) __attribute__((always_inline)) {
+    return s_wpre[i >> 5] + __popc(s_bits[i >> 5] & ((1u << (i & 31)) - 1u));
+  };
   int broken = 0;
-  {
-    Cursor cu = cur0;
-    int o0b = s_offs[cu.b], nb = s_noff[cu.b];
-#pragma unroll
-    for (int c = 0; c < kSegChunks; ++c) {
-      if ((selbits >> c) & 1u) {
-        const int i = seg0 + 64 * c + lane;
-        if (cu.advance(s_offs, B, i)) {
-          o0b = s_offs[cu.b];
-          nb = s_noff[cu.b];
-        }
-        const int k = s_row[i];
-        const int pp = p[c] == -1 ? -1 : s_row[o0b + p[c]] - nb;
-        broken |= (p[c] != -1 && pp < 0) || k >= a.capacity;   // never for a consistent selection
-        if (k < a.capacity) {
-          a.src[k] = i;
-          a.parent[k] = pp;
-        }
-      }
+  each_selected([&](int b, int o0, int i, int p) {
+    const int k = row_of(i);
+    const bool pin = p >= 0 && ((s_bits[(o0 + p) >> 5] >> ((o0 + p) & 31)) & 1u);
+    broken |= (p != -1 && !pin) || k >= a.capacity;   // never for a consistent selection
+    if (k < a.capacity) {
+      a.src[k] = i;
+      a.parent[k] = p == -1 ? -1 : (pin ? row_of(o0 + p) - s_noff[b] : -1);
     }
-  }
+  });
   if (broken) report(a.dev_err, TL_EBADTREE);
   TL_TRACE_POINT(a, 15);
 }
@@ -534,7 +559,10 @@ tl_status launch_budget_select(const BudgetArgs& a, hipStream_t stream) {
       hipFuncSetAttribute(reinterpret_cast<const void*>(select_pack_kernel),
                           hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess)
     return TL_EHIP;
-  hipLaunchKernelGGL(rho_rank_kernel, dim3((unsigned)a.batch), dim3(kRankThreads), 0, stream, a);
+  // launch 1: about kRankBlocks workgroups in all, at most one band of 64
+  // candidates each
+  const int slices = std::min(kBudgetMaxTree / 64, std::max(1, kRankBlocks / a.batch));
+  hipLaunchKernelGGL(rho_rank_kernel, dim3((unsigned)(a.batch * slices)), dim3(kRankThreads), 0, stream, a);
   hipLaunchKernelGGL(select_pack_kernel, dim3(1), dim3(kSelectThreads), lds, stream, a);
   return hipGetLastError() == hipSuccess ? TL_OK : TL_EHIP;
 }

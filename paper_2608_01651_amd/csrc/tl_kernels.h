@@ -140,6 +140,23 @@ constexpr int kBudgetMaxBatch = 1024;         // requests (one per selection thr
 constexpr int kBudgetMaxCandidates = 32768;   // candidates per batch (one workgroup's LDS)
 constexpr int kSelectThreads = 1024;
 
+// tree_budget_select's workspace, per request b (slots of max_nodes): its
+// eligible candidates' rho bits in rank order, their request-local indices,
+// its roots' indices, and {roots, eligible, rejected} counts.
+struct BudgetWorkspace {
+  size_t meta, key, cand, root, total;
+};
+inline BudgetWorkspace budget_workspace_layout(int batch, int max_nodes) {
+  BudgetWorkspace w;
+  size_t o = 0;
+  w.meta = o; o += (size_t)batch * 16;
+  w.key = o;  o += (size_t)batch * max_nodes * 4;
+  w.cand = o; o += (size_t)batch * max_nodes * 4;
+  w.root = o; o += ((size_t)batch * max_nodes * 2 + 15) / 16 * 16;
+  w.total = (o + 255) / 256 * 256;
+  return w;
+}
+
 struct BudgetArgs {
   const int32_t* cand_offsets;
   const int32_t* cand_parent;
@@ -150,6 +167,10 @@ struct BudgetArgs {
   int32_t* parent;
   int32_t* src;
   int32_t* dev_err;
+  int32_t* ws_meta;    // [batch][4]
+  uint32_t* ws_key;    // [batch][max_nodes]
+  uint32_t* ws_cand;   // [batch][max_nodes]: index | (parent + 1) << 16
+  uint16_t* ws_root;   // [batch][max_nodes]
   int batch, max_nodes, num_candidates, capacity;
 #ifdef TL_TRACE
   long long* trace;  // [blocks][16] wall-clock stamps (trace builds only)

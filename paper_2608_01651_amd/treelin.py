@@ -83,8 +83,11 @@ def lib():
         L.tree_conv_state_commit.argtypes = [P, ctypes.c_int32] + [vp] * 8
         L.tree_conv_state_commit.restype = ctypes.c_int
         L.tree_topology_export.argtypes = [P] + [vp] * 6
-        L.tree_budget_select.argtypes = [P, ctypes.c_int32, ctypes.c_int32] + [vp] * 10
+        L.tree_budget_select.argtypes = ([P, ctypes.c_int32, ctypes.c_int32] + [vp] * 9 +
+                                         [ctypes.c_size_t, vp, vp])
         L.tree_budget_select.restype = ctypes.c_int
+        L.tree_budget_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.c_int32]
+        L.tree_budget_workspace_bytes.restype = ctypes.c_size_t
         L.tree_topology_export.restype = ctypes.c_int
         L.tl_status_string.argtypes = [ctypes.c_int]
         L.tl_status_string.restype = ctypes.c_char_p
@@ -232,14 +235,27 @@ def conv_state_commit(prob, width, node_offsets, parent, terminal, x, conv_state
     _check(s, "tree_conv_state_commit")
 
 
+def budget_workspace_bytes(batch, max_nodes):
+    """tree_budget_workspace_bytes: device bytes budget_select needs."""
+    return int(lib().tree_budget_workspace_bytes(int(batch), int(max_nodes)))
+
+
+def budget_workspace(batch, max_nodes, device="cuda"):
+    """A workspace tensor for budget_select (uint8, 256-byte aligned by the allocator)."""
+    return torch.empty(max(1, budget_workspace_bytes(batch, max_nodes)), dtype=torch.uint8, device=device)
+
+
 def budget_select(prob, num_candidates, capacity, cand_offsets, cand_parent, cand_prob, rho, rank,
-                  node_offsets, parent, src, dev_err=None, stream=None):
+                  node_offsets, parent, src, workspace, dev_err=None, stream=None):
     """tree_budget_select: batch-wide allocation of `capacity` verification
     nodes over the candidate trees, packed into (node_offsets, parent, src)."""
+    if not isinstance(workspace, torch.Tensor) or not workspace.is_cuda or workspace.dtype != torch.uint8:
+        raise ValueError("workspace must be a uint8 CUDA (HIP) tensor")
     s = lib().tree_budget_select(
         ctypes.byref(prob), int(num_candidates), int(capacity),
         _ptr(cand_offsets, "cand_offsets", _I32), _ptr(cand_parent, "cand_parent", _I32),
         _ptr(cand_prob, "cand_prob", _F32), _ptr(rho, "rho", _F32), _ptr(rank, "rank", _I32),
         _ptr(node_offsets, "node_offsets", _I32), _ptr(parent, "parent", _I32),
-        _ptr(src, "src", _I32), _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
+        _ptr(src, "src", _I32), workspace.data_ptr(), workspace.numel(),
+        _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
     _check(s, "tree_budget_select")

@@ -239,21 +239,28 @@ def test_conv_entry_points_checks():
     assert _conv_commit(P(batch=0), offs=None) == tl.TL_OK
 
 
-def _budget(prob, num_candidates=64, capacity=16, **kw):
-    f = dict(offs=A16, cpar=A16, cprob=A16, rho=A16, rank=A16, no=A16, par=A16, src=A16, err=None)
+def _budget(prob, num_candidates=64, capacity=16, ws_bytes=1 << 20, **kw):
+    f = dict(offs=A16, cpar=A16, cprob=A16, rho=A16, rank=A16, no=A16, par=A16, src=A16, ws=A16,
+             err=None)
     f.update(kw)
     return _lib_or_build().tree_budget_select(
         None if prob is None else ctypes.byref(prob), num_candidates, capacity, f["offs"], f["cpar"],
-        f["cprob"], f["rho"], f["rank"], f["no"], f["par"], f["src"], f["err"], None)
+        f["cprob"], f["rho"], f["rank"], f["no"], f["par"], f["src"], f["ws"], ws_bytes, f["err"], None)
 
 
 def test_budget_select_checks():
-    assert _budget(P(batch=0), offs=None, src=None) == tl.TL_OK
+    assert _budget(P(batch=0), offs=None, src=None, ws=None) == tl.TL_OK
     assert _budget(P(), num_candidates=-1) == tl.TL_EINVAL
     assert _budget(P(), capacity=-1) == tl.TL_EINVAL
     assert _budget(P(batch=1025)) == tl.TL_EUNSUPPORTED
     assert _budget(P(), num_candidates=32769) == tl.TL_EUNSUPPORTED
-    for field in ("offs", "cpar", "cprob", "rho", "rank", "no", "par", "src"):
+    for field in ("offs", "cpar", "cprob", "rho", "rank", "no", "par", "src", "ws"):
         assert _budget(P(), **{field: None}) == tl.TL_EINVAL, field
         assert _budget(P(), **{field: MIS}) == tl.TL_EINVAL, field
+    assert _budget(P(), ws=A16 + 16) == tl.TL_EINVAL           # the workspace is 256-byte aligned
     assert _budget(P(), err=MIS) == tl.TL_EINVAL
+    need = tl.budget_workspace_bytes(2, 64)
+    assert need > 0 and need % 256 == 0
+    assert _budget(P(), ws_bytes=need - 1) == tl.TL_EINVAL
+    assert tl.budget_workspace_bytes(0, 64) == 0
+    assert tl.budget_workspace_bytes(4, 64) > tl.budget_workspace_bytes(2, 64)

@@ -36,6 +36,8 @@ class Bufs:
         self.parent = torch.zeros(max(capacity, 1), **i32)
         self.src = torch.zeros(max(capacity, 1), **i32)
         self.err = torch.zeros(1, **i32)
+        self.max_nodes = None
+        self.ws = None
 
     def load(self, offs, par, prob):
         """Eager copies of a new candidate batch; outputs poisoned."""
@@ -52,9 +54,12 @@ class Bufs:
         self.err.zero_()
 
     def launch(self, max_nodes):
+        if self.ws is None or self.max_nodes != max_nodes:   # allocate outside any capture
+            self.ws = tl.budget_workspace(self.B, max_nodes, device=H.dev())
+            self.max_nodes = max_nodes
         prob = tl.problem(self.B, 1, 1, 16, 16, max_nodes)
         tl.budget_select(prob, self.nc, self.cap, self.offs, self.cpar, self.cprob, self.rho,
-                         self.rank, self.no, self.parent, self.src, dev_err=self.err)
+                         self.rank, self.no, self.parent, self.src, self.ws, dev_err=self.err)
 
     def result(self):
         torch.cuda.synchronize()
@@ -188,6 +193,46 @@ def test_budget_bad_request_keeps_only_its_roots(kind):
         want = [int(offs[b]) + v for v in range(sl.stop - sl.start)
                 if r["rank"][v] < take]                   # root's rank is -1
         np.testing.assert_array_equal(got["src"][no[b]:no[b + 1]], want)
+
+
+def random_tree(rng, m, roots=1):
+    """m candidates, the first `roots` of them roots, every other parent drawn
+    uniformly from the candidates before it."""
+    par = np.array([-1 if v < roots else rng.integers(0, v) for v in range(m)], np.int32)
+    return par, rng.uniform(0, 1, m).astype(np.float32)
+
+
+@pytest.mark.parametrize("batch", [3, 40, 700])
+def test_budget_banded_ranking(batch):
+    """Few requests: each is ranked in bands of 64 candidates by several
+    workgroups; more than 512 requests: one workgroup per request.  Requests
+    of 1024 and 300 candidates next to small and empty ones, and a rejected
+    request of several bands that keeps only its roots."""
+    rng = np.random.default_rng(batch)
+    sizes = rng.integers(0, 40, batch)
+    sizes[0], sizes[1 % batch] = 1024, 300
+    parts = [random_tree(rng, int(m), roots=1 + int(m > 200)) for m in sizes]
+    offs, par, prob = forest_batch(parts)
+    M = int(offs[-1])
+    roots = int((par == -1).sum())
+    for capacity, max_nodes in ((roots + M // 3, 256), (roots + M // 3, 64), (M + 5, 256)):
+        print(f"banded batch={batch} M={M} capacity={capacity} max_nodes={max_nodes}", flush=True)
+        got = run(offs, par, prob, capacity, max_nodes)
+        assert_same(got, oracle.budget_select(offs, par, prob, capacity, max_nodes), f"capacity {capacity}")
+    # request 0 (1024 candidates, bands of several workgroups) is rejected
+    bad = prob.copy()
+    bad[900] = 1.5
+    print(f"banded batch={batch} rejected request 0", flush=True)
+    got = run(offs, par, bad, roots + M // 3, 256)
+    assert got["err"] == tl.TL_EINVAL
+    no = got["node_offsets"]
+    np.testing.assert_array_equal(got["src"][no[0]:no[1]], np.flatnonzero(par[:1024] == -1))
+    np.testing.assert_array_equal(got["parent"][no[0]:no[1]], -1)
+    for b in range(1, batch):
+        r = per_request_ref(offs, par, prob, b)
+        sl = slice(int(offs[b]), int(offs[b + 1]))
+        np.testing.assert_array_equal(got["rho"][sl].view(np.uint32), r["rho"].view(np.uint32))
+        np.testing.assert_array_equal(got["rank"][sl], r["rank"])
 
 
 def test_budget_batch_errors_select_nothing():
