@@ -158,22 +158,21 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
 #pragma unroll
     for (int k = 0; k < VTN; ++k) {
       const int x = tid + k * NT;
-      const int p = x & 127, cc = x >> 7;
-      v0[k] = bf16x8{};
-      v1[k] = bf16x8{};
-      if (cc < VCH && p < npair) {
-        v0[k] = *reinterpret_cast<const bf16x8*>(Vb + (size_t)(2 * p) * v_row + cc * 8);
-        if (2 * p + 1 < T) v1[k] = *reinterpret_cast<const bf16x8*>(Vb + (size_t)(2 * p + 1) * v_row + cc * 8);
-      }
+      // loaded unconditionally from clamped rows (a load under a branch is
+      // waited for where the branch ends); tasks out of range store nothing
+      const int p = min(x & 127, npair - 1), cc = min(x >> 7, VCH - 1);
+      v0[k] = *reinterpret_cast<const bf16x8*>(Vb + (size_t)(2 * p) * v_row + cc * 8);
+      v1[k] = *reinterpret_cast<const bf16x8*>(Vb + (size_t)min(2 * p + 1, T - 1) * v_row + cc * 8);
     }
 #pragma unroll
     for (int k = 0; k < VTN; ++k) {
       const int x = tid + k * NT;
       const int p = x & 127, cc = x >> 7;
       if (cc < VCH && p < npair) {
+        const bf16x8 odd = 2 * p + 1 < T ? v1[k] : bf16x8{};   // node 2p + 1, or zero past T
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          *reinterpret_cast<bf16x2*>(s_ut + (cc * 8 + e) * TS + 2 * p) = bf16x2{v0[k][e], v1[k][e]};
+          *reinterpret_cast<bf16x2*>(s_ut + (cc * 8 + e) * TS + 2 * p) = bf16x2{v0[k][e], odd[e]};
       }
     }
     // columns 2*npair .. 32*ceil(T/32)-1 are read by the last chunk: zero
