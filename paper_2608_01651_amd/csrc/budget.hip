@@ -217,8 +217,8 @@ __global__ __launch_bounds__(kRankThreads) void rho_rank_kernel(BudgetArgs a) {
   // rank = keys above mine (roots and padding have key 0: never above).
   // Work items: (64-candidate block of the band, part of the key range)
   {
-    const int nblk = (c1 - c0 + 63) >> 6;          // 1 .. 16
-    const int parts = max(1, kRankWaves / nblk);
+    const int nblk = (c1 - c0 + 63) >> 6;          // 0 (an empty request) .. 16
+    const int parts = nblk > 0 ? max(1, kRankWaves / nblk) : 1;
     const int M8 = (M + 7) & ~7;
     const int span = ((M8 / 8 + parts - 1) / parts) * 8;
     for (int it = wave; it < nblk * parts; it += kRankWaves) {   // uniform per wave
