@@ -513,10 +513,10 @@ def cpu_baseline(args, cfg, log):
                       f"{dt:.2f} s wall; CPU: {cpu_model}"}
 
 
-def calibrate_copy(log):
-    """A plain device-to-device copy of 512 MiB (torch copy_), the reference
-    kernel for scaling rocprofv3's FETCH_SIZE / WRITE_SIZE and the achievable
-    copy bandwidth (read + write bytes / time)."""
+def copy_bandwidth():
+    """A plain device-to-device copy of 512 MiB (torch copy_): bytes copied,
+    ms per copy and read + write GB/s.  It is the reference kernel for scaling
+    rocprofv3's FETCH_SIZE / WRITE_SIZE and the achievable copy bandwidth."""
     import torch
     n = (512 << 20) // 4
     src = torch.empty(n, dtype=torch.float32, device="cuda:0").uniform_()
@@ -532,9 +532,15 @@ def calibrate_copy(log):
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / reps
-    gbs = 2 * src.numel() * 4 / (ms * 1e-3) / 1e9
-    log(f"copy of {src.numel() * 4 >> 20} MiB: {ms * 1e3:.1f} us, {gbs:.0f} GB/s read+write")
-    print(json.dumps({"copy_bytes": src.numel() * 4, "copy_us": round(ms * 1e3, 2),
+    nbytes = src.numel() * 4
+    del src, dst
+    return nbytes, ms, 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def calibrate_copy(log):
+    nbytes, ms, gbs = copy_bandwidth()
+    log(f"copy of {nbytes >> 20} MiB: {ms * 1e3:.1f} us, {gbs:.0f} GB/s read+write")
+    print(json.dumps({"copy_bytes": nbytes, "copy_us": round(ms * 1e3, 2),
                       "copy_gbs": round(gbs, 1)}), flush=True)
 
 
@@ -605,7 +611,9 @@ def main():
     w = g["w"]
     ms_step = g["total_ms"] / g["steps"]
     value = w.N / (ms_step * 1e-3)
-    path_frac = (g["verify_bytes"] + g["commit_bytes"]) / (ms_step * 1e-3) / (HBM_PEAK_GBS * 1e9)
+    path_gbs = (g["verify_bytes"] + g["commit_bytes"]) / (ms_step * 1e-3) / 1e9
+    path_frac = path_gbs / HBM_PEAK_GBS
+    _, _, copy_gbs = copy_bandwidth()   # context only: the roofline is the 8 TB/s peak
     kern = {"verify": (g["verify_ms"], g["verify_bytes"]), "commit": (g["commit_ms"], g["commit_bytes"])}
     dom = max(kern, key=lambda k: kern[k][0])
     dom_ms, dom_bytes = kern[dom]
@@ -643,6 +651,8 @@ def main():
         "commit_call": "tree_state_commit_layers (all layer sets)" if args.commit_layers
                        else "tree_state_commit (one per layer set)",
         "path_hbm_frac": round(path_frac, 4),
+        "copy_context": {"copy_gbs": round(copy_gbs, 1), "path_frac_of_copy": round(path_gbs / copy_gbs, 4),
+                         "note": "a 512 MiB device copy in the same run (read + write bytes / time)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
