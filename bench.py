@@ -342,7 +342,8 @@ def conv_leg(args, cfg, log):
 def budget_bytes(M, B, N):
     """tree_budget_select: candidate parents and probabilities read once, rho
     and rank written once, node_offsets written, parent and src written per
-    packed node (the hand-offs between its three launches stay in L2)."""
+    packed node (the workspace hand-off between its two launches, at most
+    10 bytes per eligible candidate, stays in the caches and is not counted)."""
     return 8 * M + 8 * M + 4 * (B + 1) + 8 * N
 
 
