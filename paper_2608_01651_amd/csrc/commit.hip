@@ -78,12 +78,19 @@ __device__ inline int path_to_root(int term, const int* s_par, int* s_path) {
 // wait only for the former; the checks synchronise through LDS alone; the
 // gates and k/v rows of the path then go out in one round trip, and the
 // replay waits for everything.
-template <int MODE, int D, bool F32IN, bool TERMINAL>
+//
+// SPLIT workgroups share a slot: part `part` replays row blocks
+// [part * NB, part * NB + NB), NB = NRB / SPLIT (each checks the forest and
+// the path itself).
+template <int MODE, int D, bool F32IN, bool TERMINAL, int SPLIT>
 __device__ __attribute__((always_inline)) inline void commit_unit(
     const CommitCommon& a, const CommitLayer& ly, const int32_t* path_offsets,
-    const int32_t* path, const int32_t* terminal, int b, int h) {
+    const int32_t* path, const int32_t* terminal, int b, int h, int part) {
   using SH = CommitShape<D>;
   constexpr int ROWS = SH::ROWS, NRB = SH::NRB, LPR = SH::LPR, RPP = SH::RPP, PASSES = SH::PASSES;
+  static_assert(NRB % SPLIT == 0, "a slot splits into whole row blocks");
+  constexpr int NB = NRB / SPLIT;   // row blocks of this workgroup
+  const int rb0 = part * NB;
   constexpr bool GDN = (MODE == TL_MODE_GDN);
   __shared__ __align__(16) float s_k[kCommitChunk * D];
   __shared__ __align__(16) float s_v[kCommitChunk * D];
@@ -146,7 +153,7 @@ __device__ __attribute__((always_inline)) inline void commit_unit(
 #pragma unroll
     for (int p = 0; p < PASSES; ++p) {
       const int row = min(p * RPP + rsub, ROWS - 1);
-      const uint32_t o = (uint32_t)((rb * ROWS + row) * D + col) & keep;
+      const uint32_t o = (uint32_t)(((rb0 + rb) * ROWS + row) * D + col) & keep;
       st[p] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(Sp + o));
     }
   };
@@ -155,13 +162,13 @@ __device__ __attribute__((always_inline)) inline void commit_unit(
     for (int p = 0; p < PASSES; ++p) {
       const int row = p * RPP + rsub;
       if (row < ROWS)
-        __builtin_nontemporal_store(st[p], reinterpret_cast<f32x4*>(Sp + (size_t)(rb * ROWS + row) * D + col));
+        __builtin_nontemporal_store(st[p], reinterpret_cast<f32x4*>(Sp + (size_t)((rb0 + rb) * ROWS + row) * D + col));
     }
   };
   // gated linear attention keeps every block of the slot in registers (all
   // loads in flight at once); the delta rule needs more registers for its
   // row reductions and streams the blocks through two buffers
-  constexpr int NBUF = GDN ? (NRB < 2 ? NRB : 2) : NRB;
+  constexpr int NBUF = GDN ? (NB < 2 ? NB : 2) : NB;
   f32x4 sb[NBUF][PASSES];
 #pragma unroll
   for (int rb = 0; rb < NBUF; ++rb) load_block(rb, sb[rb]);
@@ -220,13 +227,12 @@ __device__ __attribute__((always_inline)) inline void commit_unit(
 #pragma unroll
       for (int p = 0; p < PASSES; ++p) {
         const int row = p * RPP + rsub;
-        const float vv = s_v[t * D + rb * ROWS + (row < ROWS ? row : 0)];
+        const float vv = s_v[t * D + (rb0 + rb) * ROWS + (row < ROWS ? row : 0)];
         if constexpr (!GDN) {
           st[p] = gam * st[p] + vv * kv;
         } else {
           float part = st[p][0] * kv[0] + st[p][1] * kv[1] + st[p][2] * kv[2] + st[p][3] * kv[3];
-#pragma unroll
-          for (int o = 1; o < LPR; o <<= 1) part += __shfl_xor(part, o, 64);
+          part = group_sum<LPR>(part);   // the row's LPR lanes
           const float u = s_beta[t] * (vv - gam * part);
           st[p] = gam * st[p] + u * kv;
         }
@@ -237,20 +243,20 @@ __device__ __attribute__((always_inline)) inline void commit_unit(
   // with the whole slot in registers, the path rows are requested only once
   // the slot has arrived: scattered row reads issued into the middle of the
   // launch-wide state stream slowed it down
-  if constexpr (NBUF == NRB) wait_vmem();
+  if constexpr (NBUF == NB) wait_vmem();
   if (Lp <= kCommitChunk) {
     stage(0, Lp);
     TL_TRACE_POINT(a, 4);
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) {
+    for (int rb = 0; rb < NB; ++rb) {
       replay(rb, Lp, sb[rb % NBUF]);
       store_block(rb, sb[rb % NBUF]);
-      if (rb + NBUF < NRB) load_block(rb + NBUF, sb[rb % NBUF]);
+      if (rb + NBUF < NB) load_block(rb + NBUF, sb[rb % NBUF]);
     }
   } else {
     // long paths: the steps are staged chunk by chunk for every block
 #pragma unroll
-    for (int rb = 0; rb < NRB; ++rb) {
+    for (int rb = 0; rb < NB; ++rb) {
       for (int c0 = 0; c0 < Lp; c0 += kCommitChunk) {
         const int n = min(kCommitChunk, Lp - c0);
         __syncthreads();   // the previous chunk is fully consumed
@@ -258,17 +264,18 @@ __device__ __attribute__((always_inline)) inline void commit_unit(
         replay(rb, n, sb[rb % NBUF]);
       }
       store_block(rb, sb[rb % NBUF]);
-      if (rb + NBUF < NRB) load_block(rb + NBUF, sb[rb % NBUF]);
+      if (rb + NBUF < NB) load_block(rb + NBUF, sb[rb % NBUF]);
     }
   }
   TL_TRACE_POINT(a, 5);
 }
 
-// One workgroup per (request, v-head) slot of one layer.
-template <int MODE, int D, bool F32IN>
+// SPLIT workgroups per (request, v-head) slot of one layer.
+template <int MODE, int D, bool F32IN, int SPLIT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void commit_kernel(CommitArgs a) {
-  commit_unit<MODE, D, F32IN, false>(a.c, a.ly, a.path_offsets, a.path, nullptr, blockIdx.x / a.c.Hv,
-                                     blockIdx.x % a.c.Hv);
+  const int slot = blockIdx.x / SPLIT, part = blockIdx.x % SPLIT;
+  commit_unit<MODE, D, F32IN, false, SPLIT>(a.c, a.ly, a.path_offsets, a.path, nullptr, slot / a.c.Hv,
+                                            slot % a.c.Hv, part);
 }
 
 // One workgroup per (layer, request, v-head) slot; consecutive workgroups
@@ -278,8 +285,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     CommitLayersArgsN<NL> a) {
   const int per_layer = a.c.batch * a.c.Hv;
   const int layer = blockIdx.x / per_layer, rem = blockIdx.x % per_layer;
-  commit_unit<MODE, D, F32IN, true>(a.c, a.ly[layer], nullptr, nullptr, a.terminal, rem / a.c.Hv,
-                                    rem % a.c.Hv);
+  commit_unit<MODE, D, F32IN, true, 1>(a.c, a.ly[layer], nullptr, nullptr, a.terminal, rem / a.c.Hv,
+                                       rem % a.c.Hv, 0);
 }
 
 // Accepted path of every request from its terminal node: path_len[b] and the
@@ -315,14 +322,41 @@ __global__ __launch_bounds__(kThreads) void accepted_path_kernel(PathArgs a) {
   if (tid < L) a.path[rq.off + tid] = s_path[tid];
 }
 
-template <int MODE, int D, bool F32IN>
-static tl_status launch_one(const CommitArgs& a, hipStream_t stream) {
-  const long blocks = (long)a.c.batch * a.c.Hv;
-  if (blocks == 0) return TL_OK;
+// Workgroups of the commit kernels that one GPU holds at once (four per
+// compute unit: 128 registers and 35 KB of LDS each).
+static long resident_commit_blocks() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  return 4L * cus;
+}
+
+template <int MODE, int D, bool F32IN, int SPLIT>
+static tl_status launch_split(const CommitArgs& a, long slots, hipStream_t stream) {
+  const long blocks = slots * SPLIT;
   if (blocks > 0x7fffffffL) return TL_EINVAL;
-  hipLaunchKernelGGL((commit_kernel<MODE, D, F32IN>), dim3((unsigned)blocks), dim3(kThreads), 0,
+  hipLaunchKernelGGL((commit_kernel<MODE, D, F32IN, SPLIT>), dim3((unsigned)blocks), dim3(kThreads), 0,
                      stream, a);
   return hipGetLastError() == hipSuccess ? TL_OK : TL_EHIP;
+}
+
+// Fewer slots than the GPU holds workgroups at once: each slot's row blocks
+// are spread over 2 or 4 workgroups (the replay is a chain of dependent
+// steps per row block, so more of them run side by side).
+template <int MODE, int D, bool F32IN>
+static tl_status launch_one(const CommitArgs& a, hipStream_t stream) {
+  const long slots = (long)a.c.batch * a.c.Hv;
+  if (slots == 0) return TL_OK;
+  constexpr int NRB = CommitShape<D>::NRB;
+  const long resident = resident_commit_blocks();
+  if constexpr (NRB % 4 == 0) {
+    if (resident > 0 && 2 * slots < resident) return launch_split<MODE, D, F32IN, 4>(a, slots, stream);
+  }
+  if constexpr (NRB % 2 == 0) {
+    if (resident > 0 && slots < resident) return launch_split<MODE, D, F32IN, 2>(a, slots, stream);
+  }
+  return launch_split<MODE, D, F32IN, 1>(a, slots, stream);
 }
 
 template <int MODE, int D, bool F32IN, int NL>
@@ -357,16 +391,6 @@ static tl_status dispatch(const tl_problem& p, const Args& a, hipStream_t stream
 
 tl_status launch_commit(const tl_problem& p, const CommitArgs& a, hipStream_t stream) {
   return dispatch(p, a, stream);
-}
-
-// Workgroups of the commit kernels that one GPU holds at once (four per
-// compute unit: 128 registers and 35 KB of LDS each).
-static long resident_commit_blocks() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-    return 0;
-  return 4L * cus;
 }
 
 // A layer whose slots alone fill the GPU goes out as a launch of its own:

@@ -187,7 +187,12 @@ __global__ __launch_bounds__(kThreads) void conv_gates_kernel(ConvArgs a) {
     float ss = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) ss += z[e] * z[e];
-    for (int o = 1; o < a.dk / 8; o <<= 1) ss += __shfl_xor(ss, o, 64);
+    switch (a.dk) {   // uniform
+      case 16: ss = group_sum<2>(ss); break;
+      case 32: ss = group_sum<4>(ss); break;
+      case 64: ss = group_sum<8>(ss); break;
+      default: ss = group_sum<16>(ss); break;
+    }
     const float scale = norm ? rsqrtf(ss + a.eps) : 1.f;
     if (live && n < T) {
       bf16x8 out;

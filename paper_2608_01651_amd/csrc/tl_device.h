@@ -2,6 +2,8 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 #include <stdint.h>
 
 #include "treelin.h"
@@ -252,6 +254,27 @@ __device__ inline void copy16_to_lds_async(const void* gsrc, void* lds_base) {
       : "=&s"(saved)
       : "v"(gsrc), "s"(m0v)
       : "memory");
+}
+
+// Sum of x over aligned groups of N lanes (N = 2, 4, 8, 16 or 32); every lane
+// of a group receives the same total.  Within a row of 16 lanes the partners
+// come from DPP (quad xor 1, quad xor 2, half-row mirror, row mirror: each
+// step adds two partial sums that cover disjoint lanes); the two rows of a
+// 32-lane group are joined by one swizzle (lane xor 16).  Every lane of the
+// wave must be active.
+template <int N>
+__device__ inline float group_sum(float x) {
+  static_assert(N == 2 || N == 4 || N == 8 || N == 16 || N == 32, "groups of 2, 4, 8, 16 or 32 lanes");
+  auto dpp = [](float v, auto ctrl) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), decltype(ctrl)::value, 0xF, 0xF, true));
+  };
+  x += dpp(x, std::integral_constant<int, 0xB1>{});   // quad_perm [1, 0, 3, 2]
+  if constexpr (N >= 4) x += dpp(x, std::integral_constant<int, 0x4E>{});   // quad_perm [2, 3, 0, 1]
+  if constexpr (N >= 8) x += dpp(x, std::integral_constant<int, 0x141>{});   // row_half_mirror
+  if constexpr (N >= 16) x += dpp(x, std::integral_constant<int, 0x140>{});  // row_mirror
+  if constexpr (N >= 32)   // bitmask swizzle: and 0x1f, or 0, xor 0x10
+    x += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), 0x401F));
+  return x;
 }
 
 // Waits for every outstanding vector memory operation of this wave
