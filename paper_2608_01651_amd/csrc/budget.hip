@@ -66,21 +66,36 @@ __device__ inline bool range_ok(int o0, int o1, int num_candidates) {
 
 __device__ inline int lane_id() { return (int)(threadIdx.x & 63); }
 
-__device__ inline int wave_sum(int x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+// Cross-lane moves by DPP (no LDS round trip).  `dpp<CTRL, ROWS>` reads the
+// source lane CTRL names; lanes without one, and rows outside the ROWS mask,
+// read 0.  Every lane of the wave must be active.
+template <int CTRL, int ROWS = 0xF>
+__device__ inline int dpp(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, ROWS, 0xF, true);
+}
+constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
+constexpr int kRowBcast15 = 0x142, kRowBcast31 = 0x143, kWaveShr1 = 0x138;
+
+// Inclusive scan over the 64 lanes: within each row of 16 lanes by shifts of
+// 1, 2, 4 and 8, then each row's total into the rows above it (lane 15 of a
+// row into the next row, lane 31 into rows 2 and 3).
+__device__ inline int wave_inclusive_scan(int x) {
+  x += dpp<kRowShr1>(x);
+  x += dpp<kRowShr2>(x);
+  x += dpp<kRowShr4>(x);
+  x += dpp<kRowShr8>(x);
+  x += dpp<kRowBcast15, 0xA>(x);
+  x += dpp<kRowBcast31, 0xC>(x);
   return x;
 }
 
-__device__ inline int wave_inclusive_scan(int x) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  return x;
+// Sum over the 64 lanes, the same in every lane.
+__device__ inline int wave_sum(int x) {
+  return __builtin_amdgcn_readlane(wave_inclusive_scan(x), 63);
 }
+
+// The value of the lane below (0 in lane 0).
+__device__ inline int lane_below(int x) { return dpp<kWaveShr1>(x); }
 
 // Sum over the workgroup (s_part: one int per wave).
 template <int NW>
@@ -293,13 +308,8 @@ __device__ inline void pick_bin(int* s_hist, uint32_t prefix, int width, int kre
   int tot = 0;
 #pragma unroll
   for (int j = 0; j < PER; ++j) tot += h[j];
-  int t = tot;   // inclusive suffix over lanes >= this one
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_down(t, o, 64);
-    if (lane + o < 64) t += y;
-  }
-  int above = t - tot;
+  const int incl = wave_inclusive_scan(tot);
+  int above = __builtin_amdgcn_readlane(incl, 63) - incl;   // the bins of the lanes above this one
 #pragma unroll
   for (int j = PER - 1; j >= 0; --j) {
     if (above < krem && krem <= above + h[j]) {   // exactly one bin satisfies this
@@ -323,8 +333,8 @@ __device__ inline void histogram_pass(const uint32_t* s_key, int E, int* s_hist,
     const uint32_t key = pos < E ? s_key[pos] : 0u;
     const bool act = pos < E && (first || (key >> (shift + width)) == prefix);
     const int digit = (int)((key >> shift) & dmask);
-    const int prev_digit = __shfl_up(digit, 1, 64);
-    const int prev_act = __shfl_up((int)act, 1, 64);
+    const int prev_digit = lane_below(digit);
+    const int prev_act = lane_below((int)act);
     const bool head = act && (lane == 0 || !prev_act || prev_digit != digit);
     const uint64_t stops = __ballot(head || !act);
     if (head) {   // the run of equal digits that starts here
