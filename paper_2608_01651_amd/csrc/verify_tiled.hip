@@ -491,7 +491,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
   // step, before that step's prefetch, so waiting for a prefetch (loaded a
   // step earlier) never waits for a store.
   bf16x8 q0[KS], q1[KS], q2[KS];   // Q fragments of tiles I, I + 1, I + 2
-  bf16x4 v0 = load_v(0), v1 = load_v(1), v2 = bf16x4{};
+  bf16x4 v0 = load_v(0), v1 = load_v(1);
   load_q(0, q0);
   load_q(1, q1);
   {
@@ -504,29 +504,24 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
 
   f32x4 pend = f32x4{0.f, 0.f, 0.f, 0.f};
   int pend_row = -1;
-  for (int I = 0; I < nt; ++I) {
-    if (I > 0) {   // rotate the prefetched rows
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        q0[ks] = q1[ks];
-        q1[ks] = q2[ks];
-      }
-      v0 = v1;
-      v1 = v2;
-    }
+  // one node tile: qa / va hold tile I, qb / vb tile I + 1, qc / vc receive
+  // tile I + 2; the three buffers change roles from tile to tile, so no
+  // prefetched register is copied (a copy would wait for its load)
+  auto tile_step = [&](int I, bf16x8 (&qa)[KS], bf16x8 (&qb)[KS], bf16x8 (&qc)[KS], bf16x4& va, bf16x4& vb,
+                       bf16x4& vc) __attribute__((always_inline)) {
     if (vw && pend_row >= 0) store_out<MODE == TL_MODE_GDN>(obase + (size_t)pend_row * v_row, pend);
     pend_row = -1;
-    load_q(I + 2, q2);   // rows clamped: harmless past the last tile
-    v2 = load_v(I + 2);
+    load_q(I + 2, qc);   // rows clamped: harmless past the last tile
+    vc = load_v(I + 2);
     if (DB && I + 1 < nt) {
       TileIn tn;
       tile_in(I + 1, tn);
-      chunks(I + 1, q1, tn, bufp(I + 1), ginp(I + 1));
+      chunks(I + 1, qb, tn, bufp(I + 1), ginp(I + 1));
     }
     if (vw) {
       TileIn t;
       tile_in(I, t);
-      pend = value_work(I, q0, v0, t, bufp(I), ginp(I));
+      pend = value_work(I, qa, va, t, bufp(I), ginp(I));
       if (kTile * I + lr < T) pend_row = kTile * I + lr;
     }
     if constexpr (DB) {
@@ -535,10 +530,16 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
       lds_barrier();   // every wave is done with the chunk buffer
       TileIn tn;
       tile_in(I + 1, tn);
-      chunks(I + 1, q1, tn, bufp(I + 1), ginp(I + 1));
+      chunks(I + 1, qb, tn, bufp(I + 1), ginp(I + 1));
       lds_barrier();   // chunks of tile I + 1 are in LDS
     }
     if (I < 2) TL_TRACE_POINT(a, 5 + I);
+  };
+  bf16x4 v2 = bf16x4{};
+  for (int I = 0; I < nt; I += 3) {   // uniform
+    tile_step(I, q0, q1, q2, v0, v1, v2);
+    if (I + 1 < nt) tile_step(I + 1, q1, q2, q0, v1, v2, v0);
+    if (I + 2 < nt) tile_step(I + 2, q2, q0, q1, v2, v0, v1);
   }
   if (vw && pend_row >= 0) store_out<MODE == TL_MODE_GDN>(obase + (size_t)pend_row * v_row, pend);
   TL_TRACE_POINT(a, 15);
