@@ -34,11 +34,23 @@
 // once, split into bf16 hi + lo in registers.
 #include <hip/hip_runtime.h>
 
+#include <utility>
+
 #include "tl_device.h"
 #include "tl_kernels.h"
 #include "verify_common.h"
 
 namespace tl {
+
+// f(std::integral_constant<int, J>{}) for J = 0 .. N-1, in order.
+template <class F, int... J>
+__device__ inline void static_for_seq(F& f, std::integer_sequence<int, J...>) {
+  (f(std::integral_constant<int, J>{}), ...);
+}
+template <int N, class F>
+__device__ inline void static_for(F& f) {
+  static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
 
 __host__ __device__ constexpr int tiled_waves(int D) { return D / kTile > kWaves ? D / kTile : kWaves; }
 
@@ -444,17 +456,21 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
 #pragma unroll
       for (int r = 0; r < 4; ++r) x[r] += t.bi * ((float)vcur[r] - Pi * sk[r]);
       // ... then the in-tile ancestors, in index order (lane (j, lg) holds u_j)
-      unsigned tin = s_tin[I];
-      while (tin) {   // uniform
-        const int j = __builtin_ffs((int)tin) - 1;
-        tin &= tin - 1;
-        const float gij = gin[lr * kTile + j];
+      // (lane j of each 16-lane row broadcast to its row by DPP row_newbcast)
+      const unsigned tin = s_tin[I];
+      auto step = [&](auto jc) __attribute__((always_inline)) {
+        constexpr int j = decltype(jc)::value;
+        if ((tin >> j) & 1u) {   // uniform
+          const float gij = gin[lr * kTile + j];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float uj = __shfl(x[r], (lg << 4) | j, 64);
-          x[r] -= gij * uj;
+          for (int r = 0; r < 4; ++r) {
+            const float uj = __int_as_float(
+                __builtin_amdgcn_update_dpp(0, __float_as_int(x[r]), 0x150 + j, 0xF, 0xF, false));
+            x[r] -= gij * uj;
+          }
         }
-      }
+      };
+      static_for<kTile>(step);
       // U_I^T -> LDS as bf16 hi + lo (zero for nodes >= T)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
