@@ -19,7 +19,8 @@
 //       X = beta (V - P (S K_I^T))               (R of Lemma 2)
 //       X -= U^T G^T over the chunks of earlier tiles (MFMA, U in hi + lo)
 //     then the in-tile part of (I + G) U = R by forward substitution over
-//     the few in-tile ancestors (lane shuffles), and U_I^T goes to LDS as
+//     the few in-tile ancestors (u_j broadcast along each 16-lane row by
+//     DPP), and U_I^T goes to LDS as
 //     bf16 hi + lo.  Only the wave's own rows of U^T are ever read back, so
 //     the solve needs no barrier: (I + G) is unit lower triangular and the
 //     tiles are solved in order (Lemma 3 bounds the depth, not needed here).
@@ -503,9 +504,9 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
   // (I + 1) & 1, free since the previous barrier) while the value work of
   // tile I reads buffer I & 1, so one barrier per tile.  Single buffer: value
   // work, barrier, chunks of the next tile, barrier.  Q rows are prefetched
-  // two tiles ahead.  Each tile's output is stored at the start of the next
-  // step, before that step's prefetch, so waiting for a prefetch (loaded a
-  // step earlier) never waits for a store.
+  // two tiles ahead into three register buffers that change roles from step
+  // to step (the tile loop is unrolled three times).  Each tile's output is
+  // stored at the start of the next step, before that step's prefetch.
   bf16x8 q0[KS], q1[KS], q2[KS];   // Q fragments of tiles I, I + 1, I + 2
   bf16x4 v0 = load_v(0), v1 = load_v(1);
   load_q(0, q0);
