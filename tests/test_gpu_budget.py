@@ -235,6 +235,39 @@ def test_budget_banded_ranking(batch):
         np.testing.assert_array_equal(got["rank"][sl], r["rank"])
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_budget_random_batches(seed):
+    """Random batches against the oracle: 1 to 700 requests (one to 16
+    workgroups per request in the ranking), trees of 0 to 1024 candidates with
+    1 to 3 roots, caps of 4 to 256 and capacities from the roots alone to
+    more than every candidate, with ties from quantised probabilities on odd
+    seeds."""
+    rng = np.random.default_rng([seed, 77])
+    batch = int(rng.choice([1, 5, 31, 130, 513, 700]))
+    sizes = rng.integers(0, 120, batch)
+    sizes[rng.integers(0, batch)] = int(rng.choice([300, 700, 1024]))
+    while sizes.sum() > 30000:
+        sizes[rng.integers(0, batch)] //= 2
+    parts = []
+    for m in sizes:
+        m = int(m)
+        roots = min(m, int(rng.integers(1, 4)))
+        par, prob = random_tree(rng, m, roots=roots)
+        if seed % 2:
+            prob = (np.round(prob * 8) / 8).astype(np.float32)
+        parts.append((par, prob))
+    offs, par, prob = forest_batch(parts)
+    M = int(offs[-1])
+    roots = int((par == -1).sum())
+    max_nodes = int(rng.choice([4, 16, 64, 256]))
+    if max(int((p == -1).sum()) for p, _ in parts) > max_nodes:
+        max_nodes = 256
+    for capacity in (roots, roots + int(rng.integers(1, max(2, M // 2))), M + 3):
+        print(f"random seed={seed} B={batch} M={M} max_nodes={max_nodes} capacity={capacity}", flush=True)
+        got = run(offs, par, prob, capacity, max_nodes)
+        assert_same(got, oracle.budget_select(offs, par, prob, capacity, max_nodes), f"capacity {capacity}")
+
+
 def test_budget_batch_errors_select_nothing():
     sizes = [((3, 2), 4), ((2, 2), 4)]
     offs, par, prob = W.make_candidates(2, sizes)
