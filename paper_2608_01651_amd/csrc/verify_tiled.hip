@@ -524,8 +524,8 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
   // one node tile: qa / va hold tile I, qb / vb tile I + 1, qc / vc receive
   // tile I + 2; the three buffers change roles from tile to tile, so no
   // prefetched register is copied (a copy would wait for its load)
-  auto tile_step = [&](int I, bf16x8 (&qa)[KS], bf16x8 (&qb)[KS], bf16x8 (&qc)[KS], bf16x4& va, bf16x4& vb,
-                       bf16x4& vc) __attribute__((always_inline)) {
+  auto tile_step = [&](int I, bf16x8 (&qa)[KS], bf16x8 (&qb)[KS], bf16x8 (&qc)[KS], bf16x4& va,
+                       [[maybe_unused]] bf16x4& vb, bf16x4& vc) __attribute__((always_inline)) {
     if (vw && pend_row >= 0) store_out<MODE == TL_MODE_GDN>(obase + (size_t)pend_row * v_row, pend);
     pend_row = -1;
     load_q(I + 2, qc);   // rows clamped: harmless past the last tile
