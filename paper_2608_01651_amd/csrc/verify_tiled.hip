@@ -56,7 +56,7 @@ __device__ inline void static_for(F& f) {
 __host__ __device__ constexpr int tiled_waves(int D) { return D / kTile > kWaves ? D / kTile : kWaves; }
 
 struct TiledLayout {
-  int cl, beta, mask, tmask, tin, gin, kst, frag, fragsz, ut, total;
+  int cl, beta, mask, tmask, tin, gin, kst, frag, fragsz, frag2, ut, total;
 };
 
 // LDS layout (bytes); identical on host and device.  With db the chunk
@@ -75,12 +75,16 @@ __host__ __device__ inline TiledLayout tiled_layout(int mode, int D, int tm, int
   L.kst = o;   o += tm * D * 2;                             // K rows, swizzled bf16
   L.frag = o;                                               // chunk operands | topology scratch
   L.fragsz = ((tm + 31) / 32) * (gdn ? 4 : 2) * 1024;       // chunks of tiles 0..I, I < tm / 16
+  // gated linear attention keeps V^T in registers once it is staged, so its
+  // second chunk buffer reuses the V^T region
+  const bool alias = !gdn && db && D * gla_vt_stride(tm) * 2 >= L.fragsz;
   {
-    const int fr = nb * L.fragsz;
+    const int fr = (alias ? 1 : nb) * L.fragsz;
     const int topo = kThreads * (4 + 4 + 4) + kThreads * W * 8;
     o += align16(fr > topo ? fr : topo);
   }
   L.ut = o;    o += D * gla_vt_stride(tm) * 2 * (gdn ? 2 : 1);   // V^T, or U^T hi and lo
+  L.frag2 = !db ? L.frag : (alias ? L.ut : L.frag + L.fragsz);   // the second chunk buffer
   L.total = o;
   return L;
 }
@@ -271,6 +275,16 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     const bf16x4 x1 = *reinterpret_cast<const bf16x4*>(p + 32);
     return bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
   };
+  // gated linear attention: the wave's V^T rows of every chunk, read once
+  // into registers (the V^T region then serves as the second chunk buffer;
+  // the barrier after the first chunks orders these reads before its use)
+  constexpr int NCH = GDN ? 1 : 2 * W;   // 32-node chunks of the largest tree
+  bf16x8 vreg[NCH];
+  if constexpr (!GDN) {
+    const int nch = (tm + 31) / 32;   // chunks that exist (uniform)
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) vreg[c] = (vw && c < nch) ? ufrag(s_ut, c) : bf16x8{};
+  }
   // chunk operands: [chunk][piece][lane] 16 bytes, pieces C hi, C lo (, -G hi, -G lo)
 
   // ---- node tiles
@@ -427,20 +441,26 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
       }
     }
     // the chunks of earlier tiles (for gated linear attention: all of them)
-    for (int c = 0; c < (GDN ? cI : cI + 1); ++c) {
-      if (!((live >> c) & 1u)) continue;   // uniform
-      ChunkOps o;
-      load_ops(c, o);
-      if constexpr (GDN) {
+    if constexpr (GDN) {
+      for (int c = 0; c < cI; ++c) {
+        if (!((live >> c) & 1u)) continue;   // uniform
+        ChunkOps o;
+        load_ops(c, o);
         x = mfma16(o.uh, o.gh, x);
         acc = mfma16(o.uh, o.ch, acc);
         x = mfma16(o.uh, o.gl, x);
         acc2 = mfma16(o.uh, o.cl, acc2);
         x = mfma16(o.ul, o.gh, x);
         acc = mfma16(o.ul, o.ch, acc);
-      } else {
-        acc = mfma16(o.uh, o.ch, acc);
-        acc = mfma16(o.uh, o.cl, acc);
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < NCH; ++c) {   // V^T from registers: a static chunk index
+        if (c > cI || !((live >> c) & 1u)) continue;   // uniform
+        const bf16x8 ch = *reinterpret_cast<const bf16x8*>(pc(c, 0));
+        const bf16x8 cl = *reinterpret_cast<const bf16x8*>(pc(c, 1));
+        acc = mfma16(vreg[c], ch, acc);
+        acc = mfma16(vreg[c], cl, acc);
       }
     }
     const float Pi = iv ? __builtin_amdgcn_exp2f(t.cli) : 0.f;
@@ -497,7 +517,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
   };
 
   // tile I's chunk operands: buffer I & 1 when double-buffered, else the only one
-  auto bufp = [&](int I) { return s_frag + (DB ? (I & 1) * L.fragsz : 0); };
+  auto bufp = [&](int I) { return (DB && (I & 1)) ? tl_lds + L.frag2 : s_frag; };
   auto ginp = [&](int I) { return s_gin + (DB ? (I & 1) * kTile * kTile : 0); };
 
   // Pipeline.  Double-buffered: step I forms the chunks of tile I + 1 (buffer

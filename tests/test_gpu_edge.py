@@ -322,6 +322,27 @@ def test_forests_with_several_roots(name, T):
     assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
 
 
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("max_nodes, sizes", [(80, [65, 80, 17]), (144, [144, 100, 70]), (256, [256, 129, 200])])
+def test_tile_walk_gla_head_dims(d, max_nodes, sizes):
+    """Gated linear attention over trees of more than 64 nodes (the tile-walk
+    kernel) at every head dimension, for buckets of 80, 144 and 256 nodes
+    (2 to 8 node chunks of 32) with ragged trees in one batch."""
+    cfg = cfg_of("large", batch=len(sizes), num_qk_heads=2, num_v_heads=4, d_k=d, d_v=d,
+                 prefix_len=0, max_nodes=max_nodes)
+    parents = [_multi_root(T, 1, 10 + k) for k, T in enumerate(sizes)]
+    paths = [chain_path(p, len(p) - 1) for p in parents]
+    w = custom(cfg, parents, paths)
+    state = rand_state(cfg, len(sizes))
+    up = H.Uploaded(w)
+    got, err = H.run_verify(cfg, up, H.t_f32(state))
+    assert err == 0
+    assert H.slice_rel_err(got, o_verify(cfg, w, state), w.node_offsets) <= H.TOL
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st) == 0
+    assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
+
+
 @pytest.mark.parametrize("name", ["large", "gdn"])
 def test_deepest_tree_256_chain(name):
     cfg = cfg_of(name, batch=1, prefix_len=0, max_nodes=256)
