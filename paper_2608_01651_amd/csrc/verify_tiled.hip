@@ -402,6 +402,10 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
   struct ChunkOps {
     bf16x8 ch, cl, gh, gl, uh, ul;
   };
+  // delta rule: U^T of every completed chunk (both of its tiles solved),
+  // this wave's rows, kept in registers once read back
+  constexpr int NCU = GDN ? 2 * W : 1;
+  bf16x8 ureg_h[NCU], ureg_l[NCU];
   auto value_work = [&](int I, const bf16x8 (&qf)[KS], const bf16x4 vcur, const TileIn& t,
                         const unsigned char* buf, const float* gin) __attribute__((always_inline)) {
     const int cI = I / 2;   // the chunk that holds tile I
@@ -442,10 +446,16 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     }
     // the chunks of earlier tiles (for gated linear attention: all of them)
     if constexpr (GDN) {
-      for (int c = 0; c < cI; ++c) {
-        if (!((live >> c) & 1u)) continue;   // uniform
+#pragma unroll
+      for (int c = 0; c < NCU; ++c) {   // completed chunks: U^T from registers
+        if (c >= cI || !((live >> c) & 1u)) continue;   // uniform
         ChunkOps o;
-        load_ops(c, o);
+        o.ch = *reinterpret_cast<const bf16x8*>(pc(c, 0));
+        o.cl = *reinterpret_cast<const bf16x8*>(pc(c, 1));
+        o.gh = *reinterpret_cast<const bf16x8*>(pc(c, 2));
+        o.gl = *reinterpret_cast<const bf16x8*>(pc(c, 3));
+        o.uh = ureg_h[c];
+        o.ul = ureg_l[c];
         x = mfma16(o.uh, o.gh, x);
         acc = mfma16(o.uh, o.ch, acc);
         x = mfma16(o.uh, o.gl, x);
@@ -508,6 +518,15 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
       acc = mfma16(uh, o.ch, acc);
       acc2 = mfma16(uh, o.cl, acc2);
       acc = mfma16(ul, o.ch, acc);
+      // chunk cI is complete after an odd tile: keep its U^T.  Every entry
+      // is rewritten (a select), so the array is only ever indexed statically
+      const bool done = (I & 1) != 0;
+#pragma unroll
+      for (int c = 0; c < NCU; ++c) {
+        const bool here = done && c == cI;
+        ureg_h[c] = here ? uh : ureg_h[c];
+        ureg_l[c] = here ? ul : ureg_l[c];
+      }
     }
     // 3. O^T = q_scale P_i B0^T + U^T C^T (U = V for gated linear attention)
     const float ps = Pi * a.q_scale;
