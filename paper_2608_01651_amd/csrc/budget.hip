@@ -352,7 +352,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_pack_kernel(BudgetArgs 
   __shared__ int s_part[kSelWaves];
   __shared__ int s_flag, s_prefix, s_krem;
   const int B = a.batch, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, mn = a.max_nodes;
-  constexpr int kGroup = 8;   // requests per wave whose lists are in flight together
+  constexpr int kGroup = 8;   // requests per wave whose lists or entries are in flight together
   int* s_hist = s_dyn;               // [kBins] (16-byte aligned: read as int4)
   int* s_offs = s_hist + kBins;      // [B + 1] candidate offsets
   int* s_roots = s_offs + B + 1;     // [B] roots
@@ -408,26 +408,40 @@ __global__ __launch_bounds__(kSelectThreads) void select_pack_kernel(BudgetArgs 
   int take = 0;   // this thread's request (tid < B): candidates taken
   if (K > 0 && K < E) {
     // -- the eligible lists, already sorted, into LDS.  A list has at most
-    // max_nodes <= 256 keys, four 64-lane chunks: a wave loads eight requests'
-    // lists at once, then stores them
-    for (int b0 = wave; b0 < B; b0 += kGroup * kSelWaves) {   // uniform per wave
-      uint32_t t[kGroup][4];
-#pragma unroll
-      for (int g = 0; g < kGroup; ++g) {
-        const int b = b0 + g * kSelWaves, n = b < B ? s_elig[b] : 0;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const int r = lane + 64 * c;
-          if (r < n) t[g][c] = a.ws_key[(size_t)b * mn + r];
-        }
+    // max_nodes <= 256 keys.  With a few requests per wave: direct copies of
+    // 64 keys per wave instruction (no registers, every list in flight at
+    // once, lanes past the list's end masked off).  With more, the direct
+    // copies issue too slowly; a wave then loads eight requests' lists at
+    // once (four 64-lane loads each) into registers and stores them.
+    if (B <= 4 * kSelWaves) {
+      for (int b = wave; b < B; b += kSelWaves) {   // uniform per wave
+        const int n = s_elig[b];
+        const uint32_t* src = a.ws_key + (size_t)b * mn;
+        uint32_t* dst = s_key + s_base[b];
+        for (int c = 0; c < n; c += 64)   // uniform
+          if (c + lane < n) copy4_to_lds_async(src + c + lane, dst + c);
       }
+      wait_vmem();   // the copies are not tracked by the compiler
+    } else {
+      for (int b0 = wave; b0 < B; b0 += kGroup * kSelWaves) {   // uniform per wave
+        uint32_t t[kGroup][4];
 #pragma unroll
-      for (int g = 0; g < kGroup; ++g) {
-        const int b = b0 + g * kSelWaves, n = b < B ? s_elig[b] : 0;
+        for (int g = 0; g < kGroup; ++g) {
+          const int b = b0 + g * kSelWaves, n = b < B ? s_elig[b] : 0;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const int r = lane + 64 * c;
-          if (r < n) s_key[s_base[b] + r] = t[g][c];
+          for (int c = 0; c < 4; ++c) {
+            const int r = lane + 64 * c;
+            if (r < n) t[g][c] = a.ws_key[(size_t)b * mn + r];
+          }
+        }
+#pragma unroll
+        for (int g = 0; g < kGroup; ++g) {
+          const int b = b0 + g * kSelWaves, n = b < B ? s_elig[b] : 0;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const int r = lane + 64 * c;
+            if (r < n) s_key[s_base[b] + r] = t[g][c];
+          }
         }
       }
     }

@@ -277,6 +277,24 @@ __device__ inline float group_sum(float x) {
   return x;
 }
 
+// The same for 4 bytes per lane (global_load_lds_dword): each active lane's
+// dword lands at lds_base + 4 * lane; inactive lanes copy nothing.
+__device__ inline void copy4_to_lds_async(const void* gsrc, void* lds_base) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds_base);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dword %1, off\n\t"
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0"
+      : "=&s"(saved)
+      : "v"(gsrc), "s"(m0v)
+      : "memory");
+}
+
 // Waits for every outstanding vector memory operation of this wave
 // (including the direct-to-LDS copies).
 __device__ inline void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
