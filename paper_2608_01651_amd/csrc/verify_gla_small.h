@@ -398,7 +398,8 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
         float* orow = obase + (size_t)i * v_row;
 #pragma unroll
         for (int m = 0; m < MT; ++m)
-          if (has_tile(m)) *reinterpret_cast<f32x4*>(orow + kTile * mtile(m) + 4 * lg) = acc[I][m] + Pi * b0[m];
+          if (has_tile(m))
+            __builtin_nontemporal_store(acc[I][m] + Pi * b0[m], reinterpret_cast<f32x4*>(orow + kTile * mtile(m) + 4 * lg));
       }
     }
   };
