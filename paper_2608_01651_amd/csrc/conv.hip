@@ -198,7 +198,7 @@ __global__ __launch_bounds__(kThreads) void conv_gates_kernel(ConvArgs a) {
       bf16x8 out;
 #pragma unroll
       for (int e = 0; e < 8; ++e) out[e] = (__bf16)(z[e] * scale);
-      *reinterpret_cast<bf16x8*>(dst0 + (size_t)(rq.off + n) * dst_row) = out;
+      __builtin_nontemporal_store(out, reinterpret_cast<bf16x8*>(dst0 + (size_t)(rq.off + n) * dst_row));
     }
   }
   TL_TRACE_POINT(a, 3);
