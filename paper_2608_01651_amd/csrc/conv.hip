@@ -92,7 +92,7 @@ __global__ __launch_bounds__(kThreads) void conv_gates_kernel(ConvArgs a) {
     const char* xg = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(a.x) + cc);
     for (int r0 = wave * NPW; r0 < T; r0 += kWaves * NPW) {
       const int r = min(r0 + lane / LPN, T - 1);
-      copy16_to_lds_async(xg + (size_t)(rq.off + r) * C * 2, s_x + r0 * CT);
+      copy16_to_lds_async<true>(xg + (size_t)(rq.off + r) * C * 2, s_x + r0 * CT);   // read once
     }
     const char* cg = reinterpret_cast<const char*>(reinterpret_cast<const __bf16*>(a.conv_state) +
                                                    (size_t)sidx * (WIDTH - 1) * C + cc);

@@ -240,20 +240,34 @@ __device__ inline void copy16_to_lds(const void* gsrc, void* lds_base) {
 // before the copied bytes are read.  M0 (the LDS base of the copy) is saved
 // and restored around it, so no register the compiler owns is changed; one
 // wait state separates each M0 write from the next instruction that reads it.
+// NT selects the non-temporal (streaming) cache policy, for data read once.
+template <bool NT = false>
 __device__ inline void copy16_to_lds_async(const void* gsrc, void* lds_base) {
   const uint32_t m0v = __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds_base);
   uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
-      "s_mov_b32 m0, %0\n\t"
-      "s_nop 0"
-      : "=&s"(saved)
-      : "v"(gsrc), "s"(m0v)
-      : "memory");
+  if constexpr (NT)
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off nt\n\t"
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0"
+        : "=&s"(saved)
+        : "v"(gsrc), "s"(m0v)
+        : "memory");
+  else
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off\n\t"
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0"
+        : "=&s"(saved)
+        : "v"(gsrc), "s"(m0v)
+        : "memory");
 }
 
 // Sum of x over aligned groups of N lanes (N = 2, 4, 8, 16 or 32); every lane
