@@ -296,6 +296,36 @@ def test_head_dims_and_groups(d, hk, hv, mode):
     assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_commit_random_batches(seed):
+    """Commit over random batches whose slot counts fall in each split of the
+    launch (under 512 slots: four workgroups per slot; under 1024: two; more:
+    one), for both rules, several head dimensions and group sizes, with empty
+    and long accepted paths."""
+    rng = np.random.default_rng([seed, 91])
+    mode = W.GDN if seed % 2 else W.GLA
+    d = int(rng.choice([32, 64, 128]))
+    hk = int(rng.choice([1, 2, 4]))
+    hv = hk * int(rng.choice([1, 2]))
+    B = int(rng.choice([3, 60, 150, 320]))
+    cfg = cfg_of("gdn" if mode == W.GDN else "production", batch=B, num_qk_heads=hk, num_v_heads=hv,
+                 d_k=d, d_v=d, prefix_len=0, max_nodes=64)
+    parents, paths = [], []
+    for b in range(B):
+        T = int(rng.integers(1, 65))
+        p = _multi_root(T, int(rng.integers(1, 3)), 1000 * seed + b)
+        parents.append(p)
+        node = int(rng.integers(-1, T))   # -1: nothing accepted
+        paths.append([] if node < 0 else chain_path(p, node))
+    w = custom(cfg, parents, paths, seed=seed)
+    state = rand_state(cfg, B, seed=seed)
+    up = H.Uploaded(w)
+    print(f"commit random seed={seed} mode={mode} d={d} Hk={hk} Hv={hv} B={B} slots={B * hv}", flush=True)
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st) == 0
+    assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
+
+
 def _multi_root(T, roots, seed):
     rng = np.random.default_rng([seed, 5])
     p = np.empty(T, np.int32)
