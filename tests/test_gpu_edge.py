@@ -326,6 +326,32 @@ def test_commit_random_batches(seed):
     assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_verify_random_batches(seed):
+    """Verify over random batches that reach every kernel of the dispatch:
+    buckets of 64, 128 and 256 nodes (the small-tree kernel, the tile walk with
+    2 and 4 mask words, and the delta rule's 129-256-node kernel at d = 128),
+    both rules, d = 32, 64 and 128, ragged trees with one to three roots."""
+    rng = np.random.default_rng([seed, 93])
+    mode = W.GDN if seed % 2 else W.GLA
+    d = int(rng.choice([32, 64, 128]))
+    max_nodes = int(rng.choice([64, 128, 256]))
+    B = int(rng.integers(1, 5))
+    cfg = cfg_of("gdn" if mode == W.GDN else "production", batch=B, num_qk_heads=2, num_v_heads=4,
+                 d_k=d, d_v=d, prefix_len=0, max_nodes=max_nodes)
+    parents = [_multi_root(int(rng.integers(1, max_nodes + 1)), int(rng.integers(1, 4)), 2000 * seed + b)
+               for b in range(B)]
+    paths = [chain_path(p, len(p) - 1) for p in parents]
+    w = custom(cfg, parents, paths, seed=seed)
+    state = rand_state(cfg, B, seed=seed)
+    up = H.Uploaded(w)
+    print(f"verify random seed={seed} mode={mode} d={d} max_nodes={max_nodes} sizes={[len(p) for p in parents]}",
+          flush=True)
+    got, err = H.run_verify(cfg, up, H.t_f32(state))
+    assert err == 0
+    assert H.slice_rel_err(got, o_verify(cfg, w, state), w.node_offsets) <= H.TOL
+
+
 def _multi_root(T, roots, seed):
     rng = np.random.default_rng([seed, 5])
     p = np.empty(T, np.int32)
