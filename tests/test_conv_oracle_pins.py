@@ -90,6 +90,24 @@ def test_gates_hand_values():
     np.testing.assert_allclose(g, -3.0 * 40.0, rtol=1e-12)
 
 
+def test_gates_bias_inside_softplus_and_signed_write_gate():
+    """The bias shifts the softplus argument: head 0 has a = 1, dt_bias = -1, so
+    softplus(0) = log 2; head 1 has a = 0, dt_bias = log(e - 1), so softplus = 1,
+    and A_log = log 2 gives g = -2.  beta = sigmoid(b): b = log 3 gives 3/4,
+    b = -log 3 gives 1/4."""
+    parent = np.array([-1, 0, 0])
+    d = case(np.random.default_rng(5), parent)
+    d["gate_a"][:] = [1.0, 0.0]
+    d["dt_bias"][:] = [-1.0, np.log(np.e - 1.0)]
+    d["A_log"][:] = [0.0, np.log(2.0)]
+    d["gate_b"][:] = [np.log(3.0), -np.log(3.0)]
+    _, _, _, g, beta = run(parent, d)
+    np.testing.assert_allclose(g[:, 0], -np.log(2.0), rtol=1e-14)
+    np.testing.assert_allclose(g[:, 1], -2.0, rtol=1e-14)
+    np.testing.assert_allclose(beta[:, 0], 0.75, rtol=1e-14)
+    np.testing.assert_allclose(beta[:, 1], 0.25, rtol=1e-14)
+
+
 def test_window_locality():
     """A node depends on its own input and its width-1 nearest ancestors only:
     changing a sibling, a descendant or an ancestor farther up leaves it
@@ -178,3 +196,26 @@ def test_pins_reject_planted_window_mistakes(monkeypatch, mut):
     monkeypatch.setattr(co, "conv_window", mut)
     with pytest.raises(AssertionError):
         test_chain_equals_numpy_convolve(4)
+
+
+# Gate mistakes are planted by editing the gate lines of a copy of the oracle's
+# source; the copy is executed as a separate module, the oracle itself is untouched.
+_GATE_LINE = "_softplus(a + np.asarray(dt_bias, np.float64)[None, :])"
+_BETA_LINE = "_sigmoid(np.asarray(gate_b, np.float64))"
+_GATE_MUTANTS = {
+    "bias_outside_softplus": (_GATE_LINE, "(_softplus(a) + np.asarray(dt_bias, np.float64)[None, :])"),
+    "bias_dropped": (_GATE_LINE, "_softplus(a)"),
+    "write_gate_sign": (_BETA_LINE, "_sigmoid(-np.asarray(gate_b, np.float64))"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(_GATE_MUTANTS))
+def test_pins_reject_planted_gate_mistakes(monkeypatch, name):
+    old, new = _GATE_MUTANTS[name]
+    src = open(co.__file__).read()
+    assert src.count(old) == 1
+    mod = {"__name__": "oracle.conv_oracle_mutant", "__package__": "oracle"}
+    exec(compile(src.replace(old, new), co.__file__, "exec"), mod)
+    monkeypatch.setattr(oracle, "conv_gates", mod["conv_gates"])
+    with pytest.raises(AssertionError):
+        test_gates_bias_inside_softplus_and_signed_write_gate()
