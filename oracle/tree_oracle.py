@@ -36,8 +36,10 @@ Conventions (readings of the paper; the kernels take the same ones)
 * Outputs are scaled by q_scale (1.0 in every workload).
 
 Parity pins: see tests/test_oracle_pins.py.  The GQA head grouping and q_scale
-are conventions the paper does not fix ("parity unpinned" for those two
-choices; both sides share them by construction).
+are conventions the paper does not fix; both sides take the same reading of
+each.  The oracle's implementation of the two is pinned against their
+definitions: grouped heads equal the ungrouped computation on qk-heads repeated
+in place (numpy.repeat), and q_scale equals scaling the queries.
 """
 from __future__ import annotations
 

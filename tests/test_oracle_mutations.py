@@ -103,3 +103,46 @@ def test_path_pins_reject_planted_mistakes(monkeypatch, mut):
     monkeypatch.setattr(to, "root_path", mut)
     with pytest.raises((AssertionError, oracle.OracleError)):
         pins.test_accepted_paths_hand_derived()
+
+
+# Mistakes outside the update step are planted by editing a copy of the
+# oracle's source, executed as a separate module; the oracle is untouched.
+_READOUT_LOOP = "            for t in root_path(pb, i):\n"
+_VERIFY_HEADS = "    hq = np.arange(Hv) // grp                  # GQA"
+_COMMIT_HEADS = "    hq = np.arange(Hv) // grp\n    new = state.copy()"
+_SOURCE_MUTANTS = {
+    "readout_before_own_update": [(_READOUT_LOOP, "            for t in root_path(pb, i)[:-1]:\n")],
+    "heads_strided": [(_VERIFY_HEADS, "    hq = np.arange(Hv) % num_qk_heads  #"),
+                      (_COMMIT_HEADS, "    hq = np.arange(Hv) % num_qk_heads\n    new = state.copy()")],
+    "query_scale_dropped": [("O[o + i] = q_scale * np.einsum", "O[o + i] = np.einsum")],
+    "query_scale_on_keys": [("O[o + i] = q_scale * np.einsum", "O[o + i] = np.einsum"),
+                            ("St = step(mode, St, k[r, hq], v[r], g[r],\n                          None if beta is None else beta[r])\n            O",
+                             "St = step(mode, St, q_scale * k[r, hq], v[r], g[r],\n                          None if beta is None else beta[r])\n            O")],
+}
+
+SOURCE_PIN_CHECKS = PIN_CHECKS + [
+    lambda: pins.test_grouped_heads_equal_repeated_qk_heads(to.GLA),
+    lambda: pins.test_grouped_heads_equal_repeated_qk_heads(to.GDN),
+    lambda: pins.test_query_scale_scales_the_queries(to.GLA),
+    lambda: pins.test_query_scale_scales_the_queries(to.GDN),
+]
+
+
+@pytest.mark.parametrize("name", sorted(_SOURCE_MUTANTS))
+def test_pins_reject_planted_source_mistake(name, monkeypatch):
+    src = open(to.__file__).read()
+    for old, new in _SOURCE_MUTANTS[name]:
+        assert src.count(old) == 1, old
+        src = src.replace(old, new)
+    mod = {"__name__": "oracle.tree_oracle_mutant", "__package__": "oracle"}
+    exec(compile(src, to.__file__, "exec"), mod)
+    for fn in ("verify", "commit"):
+        monkeypatch.setattr(oracle, fn, mod[fn])
+        monkeypatch.setattr(to, fn, mod[fn])
+    failures = 0
+    for check in SOURCE_PIN_CHECKS:
+        try:
+            check()
+        except (AssertionError, ValueError):
+            failures += 1
+    assert failures > 0, f"no pin caught {name}"

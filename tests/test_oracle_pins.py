@@ -480,3 +480,90 @@ def test_commit_layers_is_each_layer_on_the_terminal_path(mode):
         np.testing.assert_array_equal(new, want)
         np.testing.assert_array_equal(new[1], st[1])
         assert not np.allclose(new[0], st[0])
+
+
+# --------------------------------------------------------------------------
+# grouped heads and the query scale, against their definitions
+
+
+def _grouped_case(rng, mode, Hk=2, Hv=6, dk=4, dv=3):
+    parent = np.concatenate([random_parent(rng, 9), random_parent(rng, 7, roots=2)])
+    node_offsets = np.array([0, 9, 16])
+    N = parent.size
+    q = rng.standard_normal((N, Hk, dk))
+    k = rng.standard_normal((N, Hk, dk))
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    v = rng.standard_normal((N, Hv, dv))
+    g = -np.logaddexp(0, rng.standard_normal((N, Hv)))
+    beta = 1 / (1 + np.exp(-rng.standard_normal((N, Hv)))) if mode == GDN else None
+    state = 0.5 * rng.standard_normal((2, Hv, dv, dk))
+    return node_offsets, parent, q, k, v, g, beta, state
+
+
+@pytest.mark.parametrize("mode", [GLA, GDN])
+def test_grouped_heads_equal_repeated_qk_heads(mode):
+    """With Hk < Hv, each qk-head serves a run of Hv / Hk consecutive v-heads:
+    the result equals the ungrouped computation (Hk = Hv) on q and k with
+    every qk-head repeated that many times in place (numpy.repeat), for verify
+    and for commit.  v, g, beta and the state stay per v-head.  Serving the
+    groups the other way round (v-head h reading qk-head h mod Hk) differs."""
+    rng = np.random.default_rng(21)
+    Hk, Hv = 2, 6
+    node_offsets, parent, q, k, v, g, beta, state = _grouped_case(rng, mode, Hk, Hv)
+    rep = lambda t: np.repeat(t, Hv // Hk, axis=1)
+    got = oracle.verify(mode, Hk, node_offsets, parent, q, k, v, g, beta, state)
+    want = oracle.verify(mode, Hv, node_offsets, parent, rep(q), rep(k), v, g, beta, state)
+    np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-13)
+    strided = lambda t: t[:, np.arange(Hv) % Hk]
+    other = oracle.verify(mode, Hv, node_offsets, parent, strided(q), strided(k), v, g, beta, state)
+    assert not np.allclose(got, other)
+    path_offsets = np.array([0, 3, 5])
+    path = np.array(oracle.root_path(parent[:9], 8)[:3] + oracle.root_path(parent[9:], 6)[:2])
+    got = oracle.commit(mode, Hk, node_offsets, parent, path_offsets, path, k, v, g, beta, state)
+    want = oracle.commit(mode, Hv, node_offsets, parent, path_offsets, path, rep(k), v, g, beta, state)
+    np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-13)
+    assert not np.allclose(got, state)
+
+
+@pytest.mark.parametrize("mode", [GLA, GDN])
+def test_query_scale_scales_the_queries(mode):
+    """q_scale multiplies the queries and nothing else: the readout is linear in
+    q, so scaling by s equals reading out with s q at scale 1.  The state
+    update (k, v, gates) does not see it."""
+    rng = np.random.default_rng(22)
+    node_offsets, parent, q, k, v, g, beta, state = _grouped_case(rng, mode)
+    s = 0.37
+    got = oracle.verify(mode, 2, node_offsets, parent, q, k, v, g, beta, state, q_scale=s)
+    want = oracle.verify(mode, 2, node_offsets, parent, s * q, k, v, g, beta, state)
+    np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-13)
+    assert not np.allclose(got, want / s)
+
+
+def test_prefix_state_closed_forms():
+    """The chain recurrence behind S_pre, against closed forms.  Gated linear
+    attention: S_L = exp(sum g) S_0 + sum_t exp(sum_{s>t} g_s) v_t k_t^T.  Delta
+    rule with g = 0, beta = 1 and orthonormal keys: every write replaces the
+    value stored under its key, so S_L k_t = v_t for every t, and directions
+    orthogonal to all keys read S_0."""
+    rng = np.random.default_rng(23)
+    L, U, dk, dv = 7, 2, 9, 5
+    k = rng.standard_normal((L, U, dk))
+    v = rng.standard_normal((L, U, dv))
+    g = -np.logaddexp(0, rng.standard_normal((L, U)))
+    S0 = rng.standard_normal((U, dv, dk))
+    got = oracle.prefix_state(GLA, k, v, g, None, St0=S0)
+    want = np.exp(g.sum(0))[:, None, None] * S0
+    for t in range(L):
+        w = np.exp(g[t + 1:].sum(0))[:, None, None]
+        want = want + w * v[t][:, :, None] * k[t][:, None, :]
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(oracle.prefix_state(GLA, k, v, g, None),
+                               want - np.exp(g.sum(0))[:, None, None] * S0, rtol=1e-12, atol=1e-12)
+
+    basis = np.linalg.qr(rng.standard_normal((dk, dk)))[0]       # orthonormal columns
+    keys = np.stack([basis[:, :L].T] * U, axis=1)                  # [L, U, dk]
+    S = oracle.prefix_state(GDN, keys, v, np.zeros((L, U)), np.ones((L, U)), St0=S0)
+    for t in range(L):
+        np.testing.assert_allclose(np.einsum("uvk,uk->uv", S, keys[t]), v[t], atol=1e-12)
+    x = basis[:, L]                                                 # orthogonal to every key
+    np.testing.assert_allclose(S @ x, S0 @ x, atol=1e-12)
