@@ -545,7 +545,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
   // work, barrier, chunks of the next tile, barrier.  Q rows are prefetched
   // two tiles ahead into three register buffers that change roles from step
   // to step (the tile loop is unrolled three times).  Each tile's output is
-  // stored at the start of the next step, before that step's prefetch.
+  // stored in the next step, next to that step's prefetch.
   bf16x8 q0[KS], q1[KS], q2[KS];   // Q fragments of tiles I, I + 1, I + 2
   bf16x4 v0 = load_v(0), v1 = load_v(1);
   load_q(0, q0);
@@ -565,15 +565,20 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
   // prefetched register is copied (a copy would wait for its load)
   auto tile_step = [&](int I, bf16x8 (&qa)[KS], bf16x8 (&qb)[KS], bf16x8 (&qc)[KS], bf16x4& va,
                        [[maybe_unused]] bf16x4& vb, bf16x4& vc) __attribute__((always_inline)) {
-    if (vw && pend_row >= 0) store_out<MODE == TL_MODE_GDN>(obase + (size_t)pend_row * v_row, pend);
-    pend_row = -1;
-    load_q(I + 2, qc);   // rows clamped: harmless past the last tile
-    vc = load_v(I + 2);
+    // Forming the chunks of tile I + 1 consumes its Q rows, and that wait
+    // covers every load and store issued before it (one counter, which the
+    // compiler drains when both are pending).  So the output store and the
+    // prefetch of tile I + 2 are issued after it: the next step's wait then
+    // covers only work issued a whole step earlier.
     if (DB && I + 1 < nt) {
       TileIn tn;
       tile_in(I + 1, tn);
       chunks(I + 1, qb, tn, bufp(I + 1), ginp(I + 1));
     }
+    if (vw && pend_row >= 0) store_out<MODE == TL_MODE_GDN>(obase + (size_t)pend_row * v_row, pend);
+    pend_row = -1;
+    load_q(I + 2, qc);   // rows clamped: harmless past the last tile
+    vc = load_v(I + 2);
     if (vw) {
       TileIn t;
       tile_in(I, t);
