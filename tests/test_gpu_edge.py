@@ -378,6 +378,29 @@ def test_forests_with_several_roots(name, T):
     assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
 
 
+@pytest.mark.parametrize("d, max_nodes, sizes", [(128, 144, [144, 129, 40]), (128, 160, [160, 131, 90]),
+                                                  (64, 256, [256, 230, 100])])
+def test_tile_walk_delta_rule_single_buffer(d, max_nodes, sizes):
+    """The delta rule where the tile walk's layout fits LDS only with one chunk
+    buffer (node caps of 144 and 160 at d = 128, 256 at d = 64): the value work
+    and the chunks of the next tile alternate between barriers.  Ragged
+    multi-root trees, verify and commit."""
+    cfg = cfg_of("gdn", batch=len(sizes), num_qk_heads=2, num_v_heads=4, d_k=d, d_v=d,
+                 prefix_len=0, max_nodes=max_nodes)
+    parents = [_multi_root(T, 1 + k, 30 + k) for k, T in enumerate(sizes)]
+    paths = [chain_path(p, len(p) - 1) for p in parents]
+    w = custom(cfg, parents, paths, seed=d + max_nodes)
+    state = rand_state(cfg, len(sizes), seed=7)
+    up = H.Uploaded(w)
+    print(f"single-buffer tile walk d={d} max_nodes={max_nodes} sizes={sizes}", flush=True)
+    got, err = H.run_verify(cfg, up, H.t_f32(state))
+    assert err == 0
+    assert H.slice_rel_err(got, o_verify(cfg, w, state), w.node_offsets) <= H.TOL
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st) == 0
+    assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
+
+
 @pytest.mark.parametrize("d", [32, 64, 128])
 @pytest.mark.parametrize("max_nodes, sizes", [(80, [65, 80, 17]), (144, [144, 100, 70]), (256, [256, 129, 200])])
 def test_tile_walk_gla_head_dims(d, max_nodes, sizes):
