@@ -175,7 +175,7 @@ static tl_status dispatch_d(int d, const VerifyArgs& a, hipStream_t stream) {
 tl_status launch_verify(const tl_problem& p, const VerifyArgs& a, hipStream_t stream) {
   // bf16 inputs, d >= 32: gated linear attention over trees of more than 64
   // nodes, and the delta rule wherever its tile-sequential layout fits in
-  // LDS (trees of up to 128 nodes at d = 128), run node tile by node tile
+  // LDS (node caps of up to 160 at d = 128), run node tile by node tile
   // (verify_tiled.hip)
   if (p.in_dtype == TL_BF16 && p.d_k >= 32) {
     const int W = a.tm > 128 ? 4 : (a.tm > 64 ? 2 : 1);

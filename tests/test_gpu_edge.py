@@ -330,7 +330,7 @@ def test_commit_random_batches(seed):
 def test_verify_random_batches(seed):
     """Verify over random batches that reach every kernel of the dispatch:
     buckets of 64, 128 and 256 nodes (the small-tree kernel, the tile walk with
-    2 and 4 mask words, and the delta rule's 129-256-node kernel at d = 128),
+    2 and 4 mask words, and the delta rule's kernel for node caps above 160 at d = 128),
     both rules, d = 32, 64 and 128, ragged trees with one to three roots."""
     rng = np.random.default_rng([seed, 93])
     mode = W.GDN if seed % 2 else W.GLA
