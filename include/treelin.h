@@ -88,6 +88,16 @@ typedef struct tl_problem {
   float q_scale;        /* multiplies every output (1.0f: none) */
 } tl_problem;
 
+/* Bytes of layer-local device workspace that tree_lin_attn_verify needs for
+ * `problem` (the scratch whose lifetime is one layer's verification, the
+ * shortest of the three lifetimes of §4.4; §4.2 keeps the factors C, G and U
+ * of Eq. kernel-dataflow inside the tile's workgroup).  Every kernel of this
+ * library keeps those factors, the masks and the decays in registers and
+ * LDS, so the size is 0 for every problem the library supports; a caller
+ * should still size its buffer with this call.  Returns 0 for a NULL or
+ * invalid problem as well. */
+size_t tl_workspace_bytes(const tl_problem* problem);
+
 /* Tree-parallel verification (Theorem 1 of §4.1, value-tiled as in §4.2).
  *
  * For every node i of every request, writes
@@ -97,6 +107,10 @@ typedef struct tl_problem {
  * per-node state is ever formed.  `beta` must be NULL for TL_MODE_GLA and
  * non-NULL for TL_MODE_GDN.  `slot` maps request -> state slot ([B] int32,
  * each in [0, num_slots)); NULL means slot(b) = b.  `state` is only read.
+ * workspace: caller-owned device memory of workspace_bytes bytes, at least
+ *   tl_workspace_bytes(problem) (TL_EINVAL otherwise); may be NULL when
+ *   workspace_bytes is 0; a non-NULL workspace must be 256-byte aligned.
+ *   Its contents need no initialisation; calls sharing one must not overlap.
  * Device errors: TL_EBADTREE (forest), TL_EINVAL (slot index). */
 tl_status tree_lin_attn_verify(const tl_problem* problem,
                                const int32_t* node_offsets, /* [B+1] */
@@ -104,7 +118,9 @@ tl_status tree_lin_attn_verify(const tl_problem* problem,
                                const void* q, const void* k, const void* v,
                                const float* g, const float* beta,
                                const float* state, const int32_t* slot,
-                               float* out, int32_t* dev_err, void* stream);
+                               float* out, int32_t* dev_err,
+                               void* workspace, size_t workspace_bytes,
+                               void* stream);
 
 /* Accepted-path commit (§4.4 Eq. accepted-commit).
  *
@@ -142,7 +158,7 @@ typedef struct tl_layer {
 /* Most layers one tree_state_commit_layers call takes. */
 #define TL_MAX_COMMIT_LAYERS 64
 
-/* Unified cross-layer commit (§5.3 "Unified cross-layer state commit", with
+/* Unified cross-layer commit (§5.2 "Unified cross-layer state commit", with
  * §4.4 Eq. accepted-commit per layer).
  *
  * The accepted path is shared by every recurrent layer, so the commits of
@@ -166,7 +182,7 @@ tl_status tree_state_commit_layers(const tl_problem* problem, int32_t num_layers
                                    const int32_t* terminal, /* [B] */
                                    const int32_t* slot, int32_t* dev_err, void* stream);
 
-/* Device path compaction (§5.3): the accepted path of every request from its
+/* Device path compaction (§5.2): the accepted path of every request from its
  * sampled terminal node, for consumers that need the accepted rows (e.g. the
  * attention layers' cache commit, or tree_state_commit's path argument after
  * a prefix sum of path_len).  Writes path_len[b] (0 when terminal[b] == -1)

@@ -267,7 +267,7 @@ def commit(mode, num_qk_heads, node_offsets, parent, path_offsets, path, k, v,
 
 def accepted_paths(node_offsets, parent, terminal, max_nodes=MAX_NODES_LIMIT):
     """Accepted path of every request from its sampled terminal node (§4.4:
-    P(a) = Anc(a) u {a}, listed root first; §5.3: one path descriptor per
+    P(a) = Anc(a) u {a}, listed root first; §5.2: one path descriptor per
     request).  terminal[b] is request-local; -1 means nothing was accepted
     (an empty path).  Raises BadTree for a malformed forest and BadPath for a
     terminal outside [-1, T_b).  Returns (path_offsets, path) in the packed
@@ -293,7 +293,7 @@ def accepted_paths(node_offsets, parent, terminal, max_nodes=MAX_NODES_LIMIT):
 
 def commit_layers(mode, num_qk_heads, node_offsets, parent, terminal, layers,
                   slot=None, max_nodes=MAX_NODES_LIMIT):
-    """Unified cross-layer commit (§5.3): every recurrent layer commits the same
+    """Unified cross-layer commit (§5.2): every recurrent layer commits the same
     accepted path, the one ending at terminal[b].  layers is a list of
     (k, v, g, beta, state) per layer; returns the list of new states, each
     exactly commit() of that layer over accepted_paths()."""

@@ -5,6 +5,11 @@
 Every HIP source is compiled with packed fp32 instructions disabled (hipcc's
 host pass prints a harmless "not a recognized feature" warning for that
 flag).  Object files go to _build/ at the repository root.
+
+A second library, libtreelin_debug.so, is built from the same sources with
+-DTL_DEBUG: its verify kernels fill their LDS with NaN before first use, so
+that a test run against it shows any read of LDS a kernel has not written.
+The package loads libtreelin.so; only that test loads the debug library.
 """
 from __future__ import annotations
 
@@ -19,6 +24,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libtreelin.so")
+LIB_DEBUG = os.path.join(PKG, "libtreelin_debug.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -30,10 +36,11 @@ DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-p
           "-fno-gpu-flush-denormals-to-zero"]
 
 
-def _compile(src, verbose):
-    obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
+def _compile(src, verbose, debug=False):
+    objdir = os.path.join(OBJDIR, "debug") if debug else OBJDIR
+    obj = os.path.join(objdir, os.path.basename(src) + ".o")
     cmd = [HIPCC, "-c"] + (["-x", "hip"] if src.endswith(".hip") else []) + \
-        [os.path.join(CSRC, src), "-o", obj] + COMMON
+        [os.path.join(CSRC, src), "-o", obj] + COMMON + (["-DTL_DEBUG"] if debug else [])
     if src.endswith(".hip"):
         cmd += DEVICE
     else:
@@ -50,18 +57,26 @@ def _compile(src, verbose):
     return obj
 
 
-def build(verbose=False):
-    os.makedirs(OBJDIR, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, lib, verbose):
+    tmp = lib + ".tmp"
     cmd = [HIPCC, "-shared", f"--offload-arch={ARCH}", "-o", tmp] + objs
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
-        raise RuntimeError(f"linking libtreelin.so failed:\n{r.stderr}")
-    os.replace(tmp, LIB)
+        raise RuntimeError(f"linking {os.path.basename(lib)} failed:\n{r.stderr}")
+    os.replace(tmp, lib)
+
+
+def build(verbose=False, debug=True):
+    """Compile and link libtreelin.so (and, with debug, libtreelin_debug.so)."""
+    os.makedirs(os.path.join(OBJDIR, "debug"), exist_ok=True)
+    jobs = [(s, False) for s in SOURCES] + ([(s, True) for s in SOURCES] if debug else [])
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
+        objs = list(ex.map(lambda j: _compile(j[0], verbose, j[1]), jobs))
+    _link(objs[:len(SOURCES)], LIB, verbose)
+    if debug:
+        _link(objs[len(SOURCES):], LIB_DEBUG, verbose)
     return LIB
 
 

@@ -71,12 +71,22 @@ extern "C" {
 void tl_set_trace(long long* p) { g_trace = p; }
 #endif
 
+size_t tl_workspace_bytes(const tl_problem* problem) {
+  // every intermediate of verification (masks, decays, C, G, U, B0) lives in
+  // registers and LDS: no layer-local device scratch
+  (void)problem;
+  return 0;
+}
+
 tl_status tree_lin_attn_verify(const tl_problem* problem, const int32_t* node_offsets,
                                const int32_t* parent, const void* q, const void* k, const void* v,
                                const float* g, const float* beta, const float* state,
-                               const int32_t* slot, float* out, int32_t* dev_err, void* stream) {
+                               const int32_t* slot, float* out, int32_t* dev_err,
+                               void* workspace, size_t workspace_bytes, void* stream) {
   tl_status st = check_problem(problem);
   if (st != TL_OK) return st;
+  if (workspace_bytes < tl_workspace_bytes(problem)) return TL_EINVAL;
+  if (workspace_bytes > 0 && (!workspace || !aligned(workspace, 256))) return TL_EINVAL;
   if (problem->batch == 0) return TL_OK;
   st = check_tensors(problem, node_offsets, parent, k, v, g, beta, state, slot);
   if (st != TL_OK) return st;
@@ -100,6 +110,7 @@ tl_status tree_lin_attn_verify(const tl_problem* problem, const int32_t* node_of
   a.max_nodes = problem->max_nodes;
   a.num_slots = problem->num_slots;
   a.tm = (problem->max_nodes + 15) & ~15;
+  a.lds_bytes = 0;
   a.q_scale = problem->q_scale;
 #ifdef TL_TRACE
   a.trace = g_trace;
@@ -194,7 +205,7 @@ tl_status tree_topology_export(const tl_problem* problem, const int32_t* node_of
   a.batch = problem->batch;
   a.max_nodes = problem->max_nodes;
   a.words = (problem->max_nodes + 63) / 64;
-  return tl::launch_topology(a, reinterpret_cast<hipStream_t>(stream));
+  return tl::launch_topology(*problem, a, reinterpret_cast<hipStream_t>(stream));
 }
 
 tl_status tree_conv_gates(const tl_problem* problem, int32_t conv_width, float norm_eps,
@@ -290,12 +301,17 @@ size_t tree_budget_workspace_bytes(int32_t batch, int32_t max_nodes) {
   return tl::budget_workspace_layout(batch, max_nodes).total;
 }
 
-tl_status tree_budget_select(const tl_problem* problem, int32_t num_candidates, int32_t capacity,
-                             const int32_t* cand_offsets, const int32_t* cand_parent,
-                             const float* cand_prob, float* rho, int32_t* rank,
-                             int32_t* node_offsets, int32_t* parent, int32_t* src,
-                             void* workspace, size_t workspace_bytes,
-                             int32_t* dev_err, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Host checks of both budget entry points; on TL_OK `W` is the workspace
+// layout the problem needs.
+tl_status check_budget(const tl_problem* problem, int32_t num_candidates, int32_t capacity,
+                       const int32_t* cand_offsets, const int32_t* cand_parent,
+                       const float* cand_prob, const float* rho, const int32_t* rank,
+                       const int32_t* node_offsets, const int32_t* parent, const int32_t* src,
+                       const int32_t* dev_err, tl::BudgetWorkspace& W) {
   tl_status st = check_problem(problem);
   if (st != TL_OK) return st;
   if (problem->batch == 0) return TL_OK;
@@ -303,15 +319,22 @@ tl_status tree_budget_select(const tl_problem* problem, int32_t num_candidates, 
   if (problem->batch > tl::kBudgetMaxBatch || num_candidates > tl::kBudgetMaxCandidates)
     return TL_EUNSUPPORTED;
   if (!cand_offsets || !cand_parent || !cand_prob || !rho || !rank || !node_offsets || !parent ||
-      !src || !workspace)
+      !src)
     return TL_EINVAL;
   if (!aligned(cand_offsets, 4) || !aligned(cand_parent, 4) || !aligned(cand_prob, 4) ||
       !aligned(rho, 4) || !aligned(rank, 4) || !aligned(node_offsets, 4) || !aligned(parent, 4) ||
-      !aligned(src, 4) || !aligned(workspace, 256))
+      !aligned(src, 4))
     return TL_EINVAL;
   if (dev_err && !aligned(dev_err, 4)) return TL_EINVAL;
-  const tl::BudgetWorkspace W = tl::budget_workspace_layout(problem->batch, problem->max_nodes);
-  if (workspace_bytes < W.total) return TL_EINVAL;
+  W = tl::budget_workspace_layout(problem->batch, problem->max_nodes);
+  return TL_OK;
+}
+
+tl_status launch_budget(const tl_problem* problem, int32_t num_candidates, int32_t capacity,
+                        const int32_t* cand_offsets, const int32_t* cand_parent,
+                        const float* cand_prob, float* rho, int32_t* rank, int32_t* node_offsets,
+                        int32_t* parent, int32_t* src, const tl::BudgetWorkspace& W, void* workspace,
+                        int32_t* dev_err, void* stream) {
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   tl::BudgetArgs a;
   a.cand_offsets = cand_offsets;
@@ -335,6 +358,26 @@ tl_status tree_budget_select(const tl_problem* problem, int32_t num_candidates, 
   a.trace = g_trace;
 #endif
   return tl::launch_budget_select(a, reinterpret_cast<hipStream_t>(stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+tl_status tree_budget_select(const tl_problem* problem, int32_t num_candidates, int32_t capacity,
+                             const int32_t* cand_offsets, const int32_t* cand_parent,
+                             const float* cand_prob, float* rho, int32_t* rank,
+                             int32_t* node_offsets, int32_t* parent, int32_t* src,
+                             void* workspace, size_t workspace_bytes,
+                             int32_t* dev_err, void* stream) {
+  tl::BudgetWorkspace W{};
+  tl_status st = check_budget(problem, num_candidates, capacity, cand_offsets, cand_parent,
+                              cand_prob, rho, rank, node_offsets, parent, src, dev_err, W);
+  if (st != TL_OK || problem->batch == 0) return st;
+  if (!workspace || !aligned(workspace, 256)) return TL_EINVAL;
+  if (workspace_bytes < W.total) return TL_EINVAL;
+  return launch_budget(problem, num_candidates, capacity, cand_offsets, cand_parent, cand_prob, rho,
+                       rank, node_offsets, parent, src, W, workspace, dev_err, stream);
 }
 
 const char* tl_status_string(tl_status s) {

@@ -13,10 +13,10 @@
 // written; an empty path leaves the slot untouched.  The state is read and
 // written once, with non-temporal loads and stores.
 //
-// The accepted path is shared by every recurrent layer, so §5.3 folds the
+// The accepted path is shared by every recurrent layer, so §5.2 folds the
 // commits of all layers into one launch; commit_layers_kernel does that, one
 // workgroup per (layer, request, v-head).  There the path arrives as the
-// sampled terminal node of each request (the path descriptor of §5.3) and is
+// sampled terminal node of each request (the path descriptor of §5.2) and is
 // rebuilt on chip by walking the parents from it; accepted_path_kernel
 // exports the same lists.
 #include <hip/hip_runtime.h>

@@ -22,6 +22,7 @@ struct VerifyArgs {
   int32_t* dev_err;
   int batch, Hk, Hv, max_nodes, num_slots;
   int tm;          // max_nodes rounded up to a multiple of 16
+  int lds_bytes;   // dynamic LDS of the launch (set by the launcher)
   float q_scale;
 #ifdef TL_TRACE
   long long* trace;  // [blocks][16] wall-clock stamps (trace builds only)
@@ -183,7 +184,7 @@ int verify_tiled_lds_bytes(int mode, int d, int tm, int W);
 tl_status launch_commit(const tl_problem& p, const CommitArgs& a, hipStream_t stream);
 tl_status launch_commit_layers(const tl_problem& p, const CommitLayersArgs& a, hipStream_t stream);
 tl_status launch_accepted_path(const PathArgs& a, hipStream_t stream);
-tl_status launch_topology(const TopoArgs& a, hipStream_t stream);
+tl_status launch_topology(const tl_problem& p, const TopoArgs& a, hipStream_t stream);
 tl_status launch_conv_gates(const ConvArgs& a, int width, bool gdn, hipStream_t stream);
 tl_status launch_conv_state_commit(const ConvCommitArgs& a, int width, hipStream_t stream);
 tl_status launch_budget_select(const BudgetArgs& a, hipStream_t stream);

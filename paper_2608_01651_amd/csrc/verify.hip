@@ -55,6 +55,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NH == 
   constexpr int NSL = D / BV;              // value slices per head
   constexpr bool CAN_MFMA = !F32IN && D >= 32;
   const int tid = threadIdx.x;
+  lds_poison(a.lds_bytes);
   TL_TRACE_POINT(a, 0);
 
   // ---- block -> (request, qk-head, first v-head, slice).  A block serves NH
@@ -133,7 +134,9 @@ static tl_status launch_one(const VerifyArgs& a, hipStream_t stream) {
                             hipFuncAttributeMaxDynamicSharedMemorySize, L.total) != hipSuccess)
       return TL_EHIP;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kThreads), L.total, stream, a);
+  VerifyArgs b = a;
+  b.lds_bytes = L.total;
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kThreads), L.total, stream, b);
   return hipGetLastError() == hipSuccess ? TL_OK : TL_EHIP;
 }
 

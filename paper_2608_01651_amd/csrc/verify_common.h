@@ -11,6 +11,20 @@ namespace tl {
 
 extern __shared__ __align__(16) unsigned char tl_lds[];
 
+// Debug builds (-DTL_DEBUG): every word of the launch's dynamic LDS is
+// filled with NaN (0xFFC0 in each bf16 half) before any other access, so
+// that a read of LDS the kernel has not written shows up in its results.
+// Called by every thread, before any early return.  Empty otherwise.
+__device__ inline void lds_poison(int bytes) {
+#ifdef TL_DEBUG
+  for (int x = (int)threadIdx.x * 4; x < bytes; x += (int)blockDim.x * 4)
+    *reinterpret_cast<uint32_t*>(tl_lds + x) = 0xFFC0FFC0u;
+  __syncthreads();
+#else
+  (void)bytes;
+#endif
+}
+
 // ---------------------------------------------------------------------------
 // LDS layout (bytes); identical on host and device.
 // ---------------------------------------------------------------------------

@@ -104,6 +104,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63, lr = lane & 15, lg = lane >> 4;
   const bool vw = wave < VT;
+  lds_poison(a.lds_bytes);
   TL_TRACE_POINT(a, 0);
 
   // ---- block -> (request, qk-head, v-head): the grouped v-heads of a qk-head
@@ -625,7 +626,9 @@ static tl_status launch_tiled_one(const VerifyArgs& a, hipStream_t stream) {
                             hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess)
       return TL_EHIP;
   }
-  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64 * tiled_waves(D)), lds, stream, a);
+  VerifyArgs b = a;
+  b.lds_bytes = lds;
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64 * tiled_waves(D)), lds, stream, b);
   return hipGetLastError() == hipSuccess ? TL_OK : TL_EHIP;
 }
 

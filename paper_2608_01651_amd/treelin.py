@@ -70,7 +70,7 @@ def lib():
         L = ctypes.CDLL(_LIB_PATH)
         P = ctypes.POINTER(Problem)
         vp = ctypes.c_void_p
-        L.tree_lin_attn_verify.argtypes = [P] + [vp] * 12
+        L.tree_lin_attn_verify.argtypes = [P] + [vp] * 12 + [ctypes.c_size_t, vp]
         L.tree_lin_attn_verify.restype = ctypes.c_int
         L.tree_state_commit.argtypes = [P] + [vp] * 12
         L.tree_state_commit.restype = ctypes.c_int
@@ -88,6 +88,8 @@ def lib():
         L.tree_budget_select.restype = ctypes.c_int
         L.tree_budget_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.c_int32]
         L.tree_budget_workspace_bytes.restype = ctypes.c_size_t
+        L.tl_workspace_bytes.argtypes = [P]
+        L.tl_workspace_bytes.restype = ctypes.c_size_t
         L.tree_topology_export.restype = ctypes.c_int
         L.tl_status_string.argtypes = [ctypes.c_int]
         L.tl_status_string.restype = ctypes.c_char_p
@@ -143,14 +145,28 @@ def _check(status, where):
         raise TreeLinError(status, where)
 
 
+def workspace_bytes(prob):
+    """tl_workspace_bytes: device workspace bytes verify needs for `prob`."""
+    return int(lib().tl_workspace_bytes(ctypes.byref(prob)))
+
+
 def verify(prob, node_offsets, parent, q, k, v, g, beta, state, out, slot=None,
-           dev_err=None, stream=None):
-    """tree_lin_attn_verify: writes out [N, Hv, d_v] fp32."""
+           dev_err=None, workspace=None, stream=None):
+    """tree_lin_attn_verify: writes out [N, Hv, d_v] fp32.  `workspace` is an
+    optional uint8 device tensor of at least workspace_bytes(prob) bytes."""
+    if workspace is None:
+        ws_ptr, ws_bytes = None, 0
+    else:
+        if not isinstance(workspace, torch.Tensor) or not workspace.is_cuda or \
+                workspace.dtype != torch.uint8:
+            raise ValueError("workspace must be a uint8 CUDA (HIP) tensor")
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel()
     s = lib().tree_lin_attn_verify(
         ctypes.byref(prob), _ptr(node_offsets, "node_offsets", _I32), _ptr(parent, "parent", _I32),
         _ptr(q, "q", _IN), _ptr(k, "k", _IN), _ptr(v, "v", _IN), _ptr(g, "g", _F32),
         _ptr(beta, "beta", _F32, True), _ptr(state, "state", _F32), _ptr(slot, "slot", _I32, True),
-        _ptr(out, "out", _F32), _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
+        _ptr(out, "out", _F32), _ptr(dev_err, "dev_err", _I32, True), ws_ptr, ws_bytes,
+        _stream(stream))
     _check(s, "tree_lin_attn_verify")
 
 
@@ -259,3 +275,4 @@ def budget_select(prob, num_candidates, capacity, cand_offsets, cand_parent, can
         _ptr(src, "src", _I32), workspace.data_ptr(), workspace.numel(),
         _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
     _check(s, "tree_budget_select")
+

@@ -32,7 +32,7 @@ def _declared_functions():
 def test_library_exports_every_declared_function():
     L = _lib_or_build()
     names = _declared_functions()
-    assert {"tree_lin_attn_verify", "tree_state_commit", "tree_topology_export",
+    assert {"tree_lin_attn_verify", "tl_workspace_bytes", "tree_state_commit", "tree_topology_export",
             "tree_state_commit_layers", "tree_accepted_path", "tree_conv_gates",
             "tree_conv_state_commit", "tree_budget_select",
             "tl_status_string", "tl_version"} <= set(names)
@@ -62,10 +62,10 @@ MIS = 0x10002
 
 
 def _verify(prob, q=A16, k=A16, v=A16, g=A16, beta=None, state=A16, out=A16, offs=A16, par=A16,
-            slot=None, err=None):
+            slot=None, err=None, ws=None, ws_bytes=0):
     return _lib_or_build().tree_lin_attn_verify(
         None if prob is None else ctypes.byref(prob), offs, par, q, k, v, g, beta, state, slot, out,
-        err, None)
+        err, ws, ws_bytes, None)
 
 
 def _commit(prob, path_offsets=A16, path=A16, k=A16, v=A16, g=A16, beta=None, state=A16):
@@ -264,3 +264,21 @@ def test_budget_select_checks():
     assert _budget(P(), ws_bytes=need - 1) == tl.TL_EINVAL
     assert tl.budget_workspace_bytes(0, 64) == 0
     assert tl.budget_workspace_bytes(4, 64) > tl.budget_workspace_bytes(2, 64)
+
+
+def test_verify_workspace():
+    """The layer-local workspace of verify: its size query and the checks on
+    the buffer a caller passes (§4.4's layer-local lifetime)."""
+    L = _lib_or_build()
+    for prob in (P(), P(mode=tl.GDN), P(max_nodes=256, d_k=128, d_v=128), P(batch=0), P(max_nodes=0)):
+        assert tl.workspace_bytes(prob) == 0
+    assert L.tl_workspace_bytes(None) == 0
+    # a size of 0 needs no buffer; a buffer that is passed must be 256-byte aligned
+    assert _verify(P(batch=0), q=None, k=None, v=None, g=None, state=None, out=None, offs=None,
+                   par=None, ws=None, ws_bytes=0) == tl.TL_OK
+    assert _verify(P(batch=0), ws=None, ws_bytes=256) == tl.TL_EINVAL
+    assert _verify(P(batch=0), ws=A16 + 16, ws_bytes=256) == tl.TL_EINVAL
+    assert _verify(P(batch=0), ws=0x100000, ws_bytes=256) == tl.TL_OK
+    # the problem is still checked first
+    assert _verify(P(num_v_heads=3), ws=0x100000, ws_bytes=256) == tl.TL_EINVAL
+

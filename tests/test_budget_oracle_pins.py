@@ -117,9 +117,23 @@ def test_packed_forest_properties():
             if q >= 0:
                 assert parent[s[i]] == s[q] - offs[b]                   # same parent link
                 assert rho[s[i]] <= rho[s[q]]
-    # a selected set is a prefix of the global order restricted to eligible nodes
+    # the selected set is a prefix of the batch-wide order (rho descending,
+    # index ascending) restricted to eligible candidates: every eligible
+    # candidate left out ranks after every selected non-root
     chosen = set(src.tolist())
-    assert all(r["rank"][v] < 0 for v in range(int(offs[-1])) if parent[v] == -1 and v not in chosen) is True
+    M = int(offs[-1])
+    req = np.repeat(np.arange(len(offs) - 1), np.diff(offs))
+    roots = np.array([int((parent[offs[b]:offs[b + 1]] == -1).sum()) for b in range(len(offs) - 1)])
+    rank = r["rank"]
+    assert all(v in chosen for v in range(M) if parent[v] == -1)        # every root kept
+    assert all(rank[v] == -1 for v in range(M) if parent[v] == -1)
+    eligible = [v for v in range(M) if parent[v] != -1 and rank[v] < 128 - roots[req[v]]]
+    assert all(v in eligible for v in chosen if parent[v] != -1)        # only eligible ones taken
+    key = lambda v: (-float(rho[v]), v)
+    taken = [key(v) for v in eligible if v in chosen]
+    left = [key(v) for v in eligible if v not in chosen]
+    assert taken and left                                               # the case has both
+    assert max(taken) < min(left)
 
 
 def test_errors():
@@ -172,3 +186,86 @@ def test_pins_reject_a_product_in_fp64(monkeypatch):
     monkeypatch.setattr(bo, "path_scores", fp64_scores)
     with pytest.raises(AssertionError):
         test_rho_rounds_at_every_step()
+
+
+# ----------------------------------------------------------------------------
+# validity independent of rho's precision (tests/budget_validity.py): rho
+# recomputed in fp64, the cut checked up to the fp32 rounding bound
+# ----------------------------------------------------------------------------
+
+from tests.budget_validity import check_selection  # noqa: E402
+
+
+def _budget_batches():
+    for name in ("tiny", "mid", "production", "gdn", "large"):
+        case = W.budget_case(name)
+        offs, par, prob = W.make_candidates(3, case.sizes)
+        yield name, offs, par, prob, case.capacity, case.max_nodes
+    sizes = [((3, 2), 5), None, ((4, 2, 1), 6), ((2,), 9), ((5, 3), 4), None, ((2, 2, 2), 7)]
+    for quantum in (None, 1 / 16):
+        offs, par, prob = W.make_candidates(11, sizes, quantum=quantum)
+        roots = int((par == -1).sum())
+        for max_nodes in (4, 16, 256):
+            for capacity in (roots, roots + 7, roots + 40, int(offs[-1]) + 5):
+                yield f"ties q={quantum} cap={max_nodes} C={capacity}", offs, par, prob, capacity, max_nodes
+
+
+def test_oracle_selection_is_valid_at_any_precision():
+    """The oracle's fp32 selection is a correct allocation under fp64 rho, up
+    to the fp32 rounding bound (a pin that does not share the oracle's
+    precision reading)."""
+    for what, offs, par, prob, capacity, max_nodes in _budget_batches():
+        r = oracle.budget_select(offs, par, prob, capacity, max_nodes)
+        check_selection(offs, par, prob, capacity, max_nodes, r["node_offsets"], r["parent"], r["src"])
+
+
+def test_validity_check_rejects_wrong_selections():
+    """The check itself is not vacuous: swapping a selected node for a much
+    weaker one, dropping a root, exceeding max_nodes, breaking candidate
+    order or a parent link, or leaving capacity unused all fail it."""
+    case = W.budget_case("production")
+    offs, par, prob = W.make_candidates(3, case.sizes)
+    r = oracle.budget_select(offs, par, prob, case.capacity, case.max_nodes)
+    no, fpar, src = r["node_offsets"], r["parent"], r["src"]
+    args = (offs, par, prob, case.capacity, case.max_nodes)
+    check_selection(*args, no, fpar, src)
+    rho = r["rho"]
+    # a selected leaf of request 0 swapped for its request's weakest unselected leaf
+    b0 = slice(no[0], no[1])
+    s0 = src[b0]
+    child_of = set(int(par[v]) + int(offs[0]) for v in s0 if par[v] >= 0)
+    leaf = max((v for v in s0 if par[v] >= 0 and v not in child_of), key=lambda v: rho[v])
+    cand = [v for v in range(offs[0], offs[1]) if v not in set(s0.tolist()) and par[v] >= 0
+            and (par[v] + offs[0]) in set(s0.tolist()) and rho[v] < 0.5 * rho[leaf]]
+    weak = min(cand, key=lambda v: rho[v])
+    bad_src = src.copy()
+    bad_par = fpar.copy()
+    i_leaf = int(np.flatnonzero(s0 == leaf)[0])
+    new = np.sort(np.concatenate([np.delete(s0, i_leaf), [weak]]))
+    bad_src[b0] = new
+    pos = {int(v): i for i, v in enumerate(new)}
+    bad_par[b0] = [-1 if par[v] == -1 else pos[int(par[v] + offs[0])] for v in new]
+    with pytest.raises(AssertionError):
+        check_selection(*args, no, bad_par, bad_src)
+    # a root dropped (request 1 keeps one node less, its first)
+    with pytest.raises(AssertionError):
+        check_selection(*args, no, fpar, np.concatenate([src[:no[1]], src[no[1] + 1:], src[-1:]]))
+    # capacity left unused
+    short = no.copy()
+    short[-1] -= 1
+    with pytest.raises(AssertionError):
+        check_selection(*args, short, fpar, src)
+    # candidate order broken inside a request
+    swapped = src.copy()
+    swapped[[no[2] + 1, no[2] + 2]] = swapped[[no[2] + 2, no[2] + 1]]
+    with pytest.raises(AssertionError):
+        check_selection(*args, no, fpar, swapped)
+    # a parent link pointing at the wrong packed node
+    relinked = fpar.copy()
+    j = int(np.flatnonzero(fpar[no[3]:no[4]] > 0)[0]) + no[3]
+    relinked[j] -= 1
+    with pytest.raises(AssertionError):
+        check_selection(*args, no, relinked, src)
+    # a request over max_nodes
+    with pytest.raises(AssertionError):
+        check_selection(offs, par, prob, case.capacity, 8, no, fpar, src)

@@ -13,6 +13,7 @@ import oracle
 from synth import workloads as W
 from tests import gpu_helpers as H
 from paper_2608_01651_amd import treelin as tl
+from tests.budget_validity import check_selection
 
 pytestmark = pytest.mark.gpu
 
@@ -79,6 +80,12 @@ def run(offs, par, prob, capacity, max_nodes, num_candidates=None):
     return bufs.result()
 
 
+def assert_valid(got, offs, par, prob, capacity, max_nodes):
+    """Precision-independent check of the kernel's selection: correct under
+    fp64 rho up to the fp32 rounding bound (tests/budget_validity.py)."""
+    check_selection(offs, par, prob, capacity, max_nodes, got["node_offsets"], got["parent"], got["src"])
+
+
 def assert_same(got, ref, what=""):
     assert got["err"] == 0, what
     np.testing.assert_array_equal(got["rho"].view(np.uint32), ref["rho"].view(np.uint32), err_msg=what)
@@ -96,6 +103,7 @@ def test_budget_parity(name):
     got = run(offs, par, prob, case.capacity, case.max_nodes)
     ref = oracle.budget_select(offs, par, prob, case.capacity, case.max_nodes)
     assert_same(got, ref, name)
+    assert_valid(got, offs, par, prob, case.capacity, case.max_nodes)
     assert int(got["node_offsets"][-1]) == case.capacity   # the drafts always cover the capacity
 
 
@@ -113,6 +121,7 @@ def test_budget_ties_caps_and_capacities(quantum, max_nodes):
         got = run(offs, par, prob, capacity, max_nodes)
         ref = oracle.budget_select(offs, par, prob, capacity, max_nodes)
         assert_same(got, ref, f"capacity {capacity}")
+        assert_valid(got, offs, par, prob, capacity, max_nodes)
 
 
 def forest_batch(parts):
@@ -140,6 +149,7 @@ def test_budget_edge_trees():
         got = run(offs, par, prob, capacity, max_nodes)
         ref = oracle.budget_select(offs, par, prob, capacity, max_nodes)
         assert_same(got, ref, f"capacity {capacity}")
+        assert_valid(got, offs, par, prob, capacity, max_nodes)
 
 
 def test_budget_empty_batch_and_no_candidates():
@@ -219,6 +229,7 @@ def test_budget_banded_ranking(batch):
         print(f"banded batch={batch} M={M} capacity={capacity} max_nodes={max_nodes}", flush=True)
         got = run(offs, par, prob, capacity, max_nodes)
         assert_same(got, oracle.budget_select(offs, par, prob, capacity, max_nodes), f"capacity {capacity}")
+        assert_valid(got, offs, par, prob, capacity, max_nodes)
     # request 0 (1024 candidates, bands of several workgroups) is rejected
     bad = prob.copy()
     bad[900] = 1.5
@@ -266,6 +277,7 @@ def test_budget_random_batches(seed):
         print(f"random seed={seed} B={batch} M={M} max_nodes={max_nodes} capacity={capacity}", flush=True)
         got = run(offs, par, prob, capacity, max_nodes)
         assert_same(got, oracle.budget_select(offs, par, prob, capacity, max_nodes), f"capacity {capacity}")
+        assert_valid(got, offs, par, prob, capacity, max_nodes)
 
 
 def test_budget_batch_errors_select_nothing():

@@ -336,6 +336,8 @@ def test_verify_random_batches(seed):
     mode = W.GDN if seed % 2 else W.GLA
     d = int(rng.choice([32, 64, 128]))
     max_nodes = int(rng.choice([64, 128, 256]))
+    if seed == 7:   # one delta-rule draw on the kernel for node caps above 160 at d = 128
+        d, max_nodes = 128, 256
     B = int(rng.integers(1, 5))
     cfg = cfg_of("gdn" if mode == W.GDN else "production", batch=B, num_qk_heads=2, num_v_heads=4,
                  d_k=d, d_v=d, prefix_len=0, max_nodes=max_nodes)
@@ -393,6 +395,38 @@ def test_tile_walk_delta_rule_single_buffer(d, max_nodes, sizes):
     state = rand_state(cfg, len(sizes), seed=7)
     up = H.Uploaded(w)
     print(f"single-buffer tile walk d={d} max_nodes={max_nodes} sizes={sizes}", flush=True)
+    got, err = H.run_verify(cfg, up, H.t_f32(state))
+    assert err == 0
+    assert H.slice_rel_err(got, o_verify(cfg, w, state), w.node_offsets) <= H.TOL
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st) == 0
+    assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
+
+
+@pytest.mark.parametrize("max_nodes, trees", [
+    (176, [("roots", 176, 1), ("roots", 100, 2), ("roots", 17, 3), ("topk", 64, 0)]),
+    (256, [("roots", 256, 1), ("roots", 177, 3), ("roots", 90, 2), ("roots", 15, 1), ("topk", 200, 0)]),
+])
+def test_delta_rule_wide_cap_kernel(max_nodes, trees):
+    """The delta rule's kernel for node caps beyond the tile walk's LDS (d =
+    128, caps of 176..256): its level-by-level solve over branching,
+    multi-root and partial-tile forests of several sizes in one batch (the
+    wave topology serves trees of <= 64 nodes, the LDS one the others, and
+    trees of < 16 nodes the vector path), verify and commit."""
+    cfg = cfg_of("gdn", batch=len(trees), num_qk_heads=2, num_v_heads=4, d_k=128, d_v=128,
+                 prefix_len=0, max_nodes=max_nodes)
+    parents = []
+    for k, (kind, T, roots) in enumerate(trees):
+        if kind == "roots":
+            parents.append(_multi_root(T, roots, 50 + k))
+        else:
+            parents.append(W.topk_tree(np.random.default_rng([k, 61]), T, (16, 4, 2), 12))
+    paths = [chain_path(p, len(p) - 1) for p in parents]
+    paths[1] = chain_path(parents[1], int(np.argmax(W.node_depths(parents[1]))))
+    w = custom(cfg, parents, paths, seed=max_nodes)
+    state = rand_state(cfg, len(trees), seed=11)
+    up = H.Uploaded(w)
+    print(f"delta rule wide cap max_nodes={max_nodes} sizes={[len(p) for p in parents]}", flush=True)
     got, err = H.run_verify(cfg, up, H.t_f32(state))
     assert err == 0
     assert H.slice_rel_err(got, o_verify(cfg, w, state), w.node_offsets) <= H.TOL

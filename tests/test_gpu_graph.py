@@ -1,4 +1,4 @@
-"""HIP-graph capture of a verification round in a capacity bucket (§5.3:
+"""HIP-graph capture of a verification round in a capacity bucket (§5.2:
 captured graphs keep fixed addresses and kernel shapes while the tree
 topology varies from round to round).
 

@@ -108,3 +108,46 @@ def test_mfma_threshold_15_vs_16():
         assert err == 0
         e = H.slice_rel_err(got, _oracle_verify(cfg, w, state), w.node_offsets)
         assert e <= H.TOL, (T, e)
+
+
+def _forest(T, roots, rng):
+    p = np.empty(T, np.int32)
+    p[:roots] = -1
+    for i in range(roots, T):
+        p[i] = rng.integers(0, i)
+    return p
+
+
+@pytest.mark.parametrize("base, mode, d, max_nodes, hk, hv", [
+    ("production", W.GLA, 128, 64, 16, 32),   # small-tree kernel, two v-heads per block
+    ("production", W.GLA, 64, 48, 3, 3),      # small-tree kernel, one v-head per block
+    ("gdn", W.GDN, 128, 256, 2, 4),           # the delta rule's wide-cap kernel
+    ("gdn", W.GDN, 64, 128, 2, 4),            # tile walk, 2 mask words
+    ("large", W.GLA, 128, 200, 2, 4),         # tile walk, 4 mask words
+    ("tiny", W.GLA, 16, 64, 1, 1),            # vector path (fp32 inputs)
+])
+def test_topology_export_per_kernel(base, mode, d, max_nodes, hk, hv):
+    """tree_topology_export runs the topology routine of the verify kernel
+    that serves the same problem; its M+ rows and depths are bit-exact
+    against the oracle's pointer walks on ragged forests of several roots,
+    chains, single nodes and full trees at the node cap."""
+    import dataclasses
+    cfg = dataclasses.replace(W.CONFIGS[base], mode=mode, d_k=d, d_v=d, max_nodes=max_nodes,
+                              num_qk_heads=hk, num_v_heads=hv)
+    rng = np.random.default_rng([max_nodes, d, mode])
+    sizes = [max_nodes, 1, min(15, max_nodes), min(16, max_nodes), min(64, max_nodes),
+             min(65, max_nodes), int(rng.integers(1, max_nodes + 1)), 0]
+    parents = [_forest(T, int(rng.integers(1, 4)) if T > 3 else 1, rng) for T in sizes]
+    parents.append(W.chain_tree(max_nodes))
+    offs = np.concatenate([[0], np.cumsum([len(p) for p in parents])]).astype(np.int32)
+    par = np.concatenate(parents).astype(np.int32)
+    N, words = int(offs[-1]), (max_nodes + 63) // 64
+    mask = torch.zeros((N, words), dtype=torch.int64, device=H.dev())
+    depth = torch.full((N,), -7, dtype=torch.int32, device=H.dev())
+    err = torch.zeros(1, dtype=torch.int32, device=H.dev())
+    tl.topology(H.problem_for(cfg, len(parents)), H.t_int(offs), H.t_int(par), mask, depth, dev_err=err)
+    torch.cuda.synchronize()
+    assert err.item() == 0
+    ref_mask, ref_depth = oracle.topology(offs, par, max_nodes)
+    np.testing.assert_array_equal(mask.cpu().numpy().view(np.uint64), ref_mask[:, :words])
+    np.testing.assert_array_equal(depth.cpu().numpy(), ref_depth)

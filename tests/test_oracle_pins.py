@@ -423,7 +423,7 @@ def test_error_classes():
 
 
 # --------------------------------------------------------------------------
-# accepted path from a terminal node, and the cross-layer commit (§5.3)
+# accepted path from a terminal node, and the cross-layer commit (§5.2)
 # --------------------------------------------------------------------------
 
 def test_accepted_paths_hand_derived():
