@@ -294,6 +294,32 @@ tl_status tree_budget_select(const tl_problem* problem, int32_t num_candidates, 
  * and a per-request bound of `max_nodes` nodes (0 for an empty batch). */
 size_t tree_budget_workspace_bytes(int32_t batch, int32_t max_nodes);
 
+/* Largest workspace tree_budget_select_noalloc can serve: 1 MiB, i.e.
+ * tree_budget_workspace_bytes(batch, max_nodes) <= this, which holds e.g. for
+ * batch <= 1024 at max_nodes <= 100 and batch <= 407 at max_nodes = 256. */
+#define TL_BUDGET_NOALLOC_MAX_BYTES (1u << 20)
+
+/* tree_budget_select without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, results and errors as
+ * tree_budget_select minus workspace and workspace_bytes: the workspace is a
+ * static device array of TL_BUDGET_NOALLOC_MAX_BYTES bytes inside the
+ * library, one per GPU, held until the process ends.  Nothing is allocated
+ * on any call (the first call on a device looks up that device's array).
+ * A problem whose workspace would exceed it returns TL_EUNSUPPORTED before
+ * anything is enqueued.  Every call on one GPU shares that GPU's array, so
+ * calls that overlap on one GPU (several streams, several threads) race;
+ * calls on one stream are ordered and safe.  The array needs no clearing:
+ * each call writes every entry it later reads. */
+tl_status tree_budget_select_noalloc(const tl_problem* problem, int32_t num_candidates,
+                                     int32_t capacity,
+                                     const int32_t* cand_offsets, const int32_t* cand_parent,
+                                     const float* cand_prob,
+                                     float* rho, int32_t* rank,     /* [num_candidates] out */
+                                     int32_t* node_offsets,         /* [B+1] out */
+                                     int32_t* parent, int32_t* src, /* [capacity] out */
+                                     int32_t* dev_err, void* stream);
+
 /* Tree topology of §4.1's notation table, as the kernels build it:
  * anc_mask[r, w] (W = ceil(max_nodes/64) uint64 words per node) has bit
  * (j mod 64) of word j/64 set iff local node j is r's node itself or one of

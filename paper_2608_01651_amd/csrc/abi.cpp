@@ -380,6 +380,24 @@ tl_status tree_budget_select(const tl_problem* problem, int32_t num_candidates, 
                        rank, node_offsets, parent, src, W, workspace, dev_err, stream);
 }
 
+tl_status tree_budget_select_noalloc(const tl_problem* problem, int32_t num_candidates,
+                                     int32_t capacity, const int32_t* cand_offsets,
+                                     const int32_t* cand_parent, const float* cand_prob,
+                                     float* rho, int32_t* rank, int32_t* node_offsets,
+                                     int32_t* parent, int32_t* src, int32_t* dev_err,
+                                     void* stream) {
+  tl::BudgetWorkspace W{};
+  tl_status st = check_budget(problem, num_candidates, capacity, cand_offsets, cand_parent,
+                              cand_prob, rho, rank, node_offsets, parent, src, dev_err, W);
+  if (st != TL_OK || problem->batch == 0) return st;
+  if (W.total > tl::kBudgetScratchBytes) return TL_EUNSUPPORTED;   // beyond the static buffer
+  void* ws = nullptr;
+  st = tl::budget_scratch(&ws);
+  if (st != TL_OK) return st;
+  return launch_budget(problem, num_candidates, capacity, cand_offsets, cand_parent, cand_prob, rho,
+                       rank, node_offsets, parent, src, W, ws, dev_err, stream);
+}
+
 const char* tl_status_string(tl_status s) {
   switch (s) {
     case TL_OK: return "TL_OK: success";

@@ -42,11 +42,40 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "tl_device.h"
 #include "tl_kernels.h"
 
+// The workspace of tree_budget_select_noalloc: one copy per GPU, held until
+// the process ends.  In host code `scratch` names a host-side stand-in, not
+// device memory: only the address hipGetSymbolAddress returns for the
+// current device may be handed to kernels or copies.
+static __device__ __align__(256) unsigned char scratch[tl::kBudgetScratchBytes];
+
 namespace tl {
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};   // device address of `scratch`, per device
+}  // namespace
+
+// Device address of the current device's copy of `scratch`: looked up once
+// per device, with that device current, and kept.
+tl_status budget_scratch(void** ptr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return TL_EHIP;
+  if (dev < 0 || dev >= kMaxDevices) return TL_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return TL_EHIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return TL_OK;
+}
 
 namespace {
 

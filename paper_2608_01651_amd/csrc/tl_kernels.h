@@ -141,6 +141,9 @@ constexpr int kBudgetMaxBatch = 1024;         // requests (one per selection thr
 constexpr int kBudgetMaxCandidates = 32768;   // candidates per batch (one workgroup's LDS)
 constexpr int kSelectThreads = 1024;
 
+// Bytes of the static workspace of tree_budget_select_noalloc (per GPU).
+constexpr size_t kBudgetScratchBytes = TL_BUDGET_NOALLOC_MAX_BYTES;
+
 // tree_budget_select's workspace, per request b (slots of max_nodes): its
 // eligible candidates' rho bits in rank order, their request-local indices,
 // its roots' indices, and {roots, eligible, rejected} counts.
@@ -188,6 +191,9 @@ tl_status launch_topology(const tl_problem& p, const TopoArgs& a, hipStream_t st
 tl_status launch_conv_gates(const ConvArgs& a, int width, bool gdn, hipStream_t stream);
 tl_status launch_conv_state_commit(const ConvCommitArgs& a, int width, hipStream_t stream);
 tl_status launch_budget_select(const BudgetArgs& a, hipStream_t stream);
+// Device address of the current device's static budget workspace (the
+// kBudgetScratchBytes array of tree_budget_select_noalloc).
+tl_status budget_scratch(void** ptr);
 int budget_select_lds_bytes(int batch, int num_candidates);
 int verify_lds_bytes(const tl_problem& p, int tm);
 

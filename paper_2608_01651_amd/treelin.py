@@ -49,6 +49,7 @@ class Layer(ctypes.Structure):
 
 
 MAX_COMMIT_LAYERS = 64
+BUDGET_NOALLOC_MAX_BYTES = 1 << 20   # TL_BUDGET_NOALLOC_MAX_BYTES
 
 
 def problem(batch, num_qk_heads, num_v_heads, d_k, d_v, max_nodes, num_slots=None,
@@ -86,6 +87,8 @@ def lib():
         L.tree_budget_select.argtypes = ([P, ctypes.c_int32, ctypes.c_int32] + [vp] * 9 +
                                          [ctypes.c_size_t, vp, vp])
         L.tree_budget_select.restype = ctypes.c_int
+        L.tree_budget_select_noalloc.argtypes = [P, ctypes.c_int32, ctypes.c_int32] + [vp] * 10
+        L.tree_budget_select_noalloc.restype = ctypes.c_int
         L.tree_budget_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.c_int32]
         L.tree_budget_workspace_bytes.restype = ctypes.c_size_t
         L.tl_workspace_bytes.argtypes = [P]
@@ -276,3 +279,15 @@ def budget_select(prob, num_candidates, capacity, cand_offsets, cand_parent, can
         _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
     _check(s, "tree_budget_select")
 
+
+def budget_select_noalloc(prob, num_candidates, capacity, cand_offsets, cand_parent, cand_prob,
+                          rho, rank, node_offsets, parent, src, dev_err=None, stream=None):
+    """tree_budget_select_noalloc: budget_select with the library's static
+    per-GPU workspace (no allocation; calls overlapping on one GPU race)."""
+    s = lib().tree_budget_select_noalloc(
+        ctypes.byref(prob), int(num_candidates), int(capacity),
+        _ptr(cand_offsets, "cand_offsets", _I32), _ptr(cand_parent, "cand_parent", _I32),
+        _ptr(cand_prob, "cand_prob", _F32), _ptr(rho, "rho", _F32), _ptr(rank, "rank", _I32),
+        _ptr(node_offsets, "node_offsets", _I32), _ptr(parent, "parent", _I32),
+        _ptr(src, "src", _I32), _ptr(dev_err, "dev_err", _I32, True), _stream(stream))
+    _check(s, "tree_budget_select_noalloc")

@@ -170,6 +170,23 @@ int main() {
     CHECK(inside(a.ws_cand, 128 * 256 * 4) && inside(a.ws_root, 128 * 256 * 2));
     CHECK(a.capacity == 8192 && a.num_candidates == 20000 && a.max_nodes == 256);
   }
+  // ---- budget allocation without a workspace: refused beyond the static
+  // buffer before any lookup; otherwise the static buffer is used
+  const int lookups = stub::calls.scratch;
+  tl_problem big = problem(408, 1, 1, 16, 256, TL_MODE_GLA);
+  auto noalloc = [&](const tl_problem* q) {
+    return tree_budget_select_noalloc(q, 20000, 8192, F<const int32_t>(0x1000), F<const int32_t>(0x2000),
+                                      F<const float>(0x3000), F<float>(0x4000), F<int32_t>(0x5000),
+                                      F<int32_t>(0x6000), F<int32_t>(0x7000), F<int32_t>(0x8000), nullptr,
+                                      nullptr);
+  };
+  CHECK(noalloc(&big) == TL_EUNSUPPORTED);
+  CHECK(stub::calls.scratch == lookups);
+  stub::calls.scratch_base = P(0x2000000);
+  CHECK(noalloc(&pb) == TL_OK);
+  CHECK(stub::calls.scratch == lookups + 1);
+  CHECK((uintptr_t)stub::calls.budget_args.ws_meta == 0x2000000);
+  CHECK((uintptr_t)stub::calls.budget_args.ws_root + 128 * 256 * 2 <= 0x2000000 + TL_BUDGET_NOALLOC_MAX_BYTES);
 
   if (failures) {
     std::fprintf(stderr, "%d check(s) failed\n", failures);

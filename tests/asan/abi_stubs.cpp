@@ -56,4 +56,10 @@ tl_status launch_budget_select(const BudgetArgs& a, hipStream_t) {
   stub::calls.budget_args = a;
   return TL_OK;
 }
+tl_status budget_scratch(void** ptr) {
+  stub::calls.scratch++;
+  *ptr = stub::calls.scratch_base;
+  return TL_OK;
+}
+
 }  // namespace tl

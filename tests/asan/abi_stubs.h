@@ -6,7 +6,7 @@
 namespace stub {
 struct Calls {
   int verify = 0, commit = 0, commit_layers = 0, path = 0, topology = 0, conv = 0,
-      conv_commit = 0, budget = 0;
+      conv_commit = 0, budget = 0, scratch = 0;
   tl_problem problem{};
   tl::VerifyArgs verify_args{};
   tl::CommitArgs commit_args{};
@@ -18,6 +18,7 @@ struct Calls {
   bool conv_gdn = false;
   int conv_commit_tiles = -1;
   tl::BudgetArgs budget_args{};
+  void* scratch_base = nullptr;
 };
 extern Calls calls;
 }  // namespace stub

@@ -282,3 +282,30 @@ def test_verify_workspace():
     # the problem is still checked first
     assert _verify(P(num_v_heads=3), ws=0x100000, ws_bytes=256) == tl.TL_EINVAL
 
+
+def _budget_noalloc(prob, num_candidates=64, capacity=16, **kw):
+    f = dict(offs=A16, cpar=A16, cprob=A16, rho=A16, rank=A16, no=A16, par=A16, src=A16, err=None)
+    f.update(kw)
+    return _lib_or_build().tree_budget_select_noalloc(
+        None if prob is None else ctypes.byref(prob), num_candidates, capacity, f["offs"], f["cpar"],
+        f["cprob"], f["rho"], f["rank"], f["no"], f["par"], f["src"], f["err"], None)
+
+
+def test_budget_select_noalloc_checks():
+    """The allocation-free budget entry point: the same host checks as
+    tree_budget_select, and a problem whose workspace exceeds the static
+    buffer is refused before anything is enqueued."""
+    assert _budget_noalloc(None) == tl.TL_EINVAL
+    assert _budget_noalloc(P(batch=0), offs=None, src=None) == tl.TL_OK
+    assert _budget_noalloc(P(), num_candidates=-1) == tl.TL_EINVAL
+    assert _budget_noalloc(P(batch=1025)) == tl.TL_EUNSUPPORTED
+    for field in ("offs", "cpar", "cprob", "rho", "rank", "no", "par", "src"):
+        assert _budget_noalloc(P(), **{field: None}) == tl.TL_EINVAL, field
+        assert _budget_noalloc(P(), **{field: MIS}) == tl.TL_EINVAL, field
+    assert _budget_noalloc(P(), err=MIS) == tl.TL_EINVAL
+    # the static buffer's bound: the largest shapes that fit, and the first that do not
+    assert tl.budget_workspace_bytes(1024, 100) <= tl.BUDGET_NOALLOC_MAX_BYTES
+    assert tl.budget_workspace_bytes(1024, 101) > tl.BUDGET_NOALLOC_MAX_BYTES
+    assert tl.budget_workspace_bytes(407, 256) <= tl.BUDGET_NOALLOC_MAX_BYTES
+    assert _budget_noalloc(P(batch=1024, max_nodes=101)) == tl.TL_EUNSUPPORTED
+    assert _budget_noalloc(P(batch=408, max_nodes=256)) == tl.TL_EUNSUPPORTED
