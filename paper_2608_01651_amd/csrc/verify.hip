@@ -176,6 +176,10 @@ static tl_status dispatch_d(int d, const VerifyArgs& a, hipStream_t stream) {
 }
 
 tl_status launch_verify(const tl_problem& p, const VerifyArgs& a, hipStream_t stream) {
+  // the delta rule at d = 128 over node caps of up to 128: the correction
+  // system inverted once per workgroup (verify_gdn_dense.hip)
+  if (p.mode == TL_MODE_GDN && p.in_dtype == TL_BF16 && p.d_k == 128 && a.tm <= 128)
+    return launch_verify_gdn_dense(p, a, stream);
   // bf16 inputs, d >= 32: gated linear attention over trees of more than 64
   // nodes, and the delta rule wherever its tile-sequential layout fits in
   // LDS (node caps of up to 160 at d = 128), run node tile by node tile

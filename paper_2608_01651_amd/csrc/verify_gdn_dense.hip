@@ -1,0 +1,587 @@
+// Verify, gated delta rule on MFMA, trees of up to 128 nodes at d = 128:
+// the correction system solved once per workgroup as an explicit inverse,
+// so that the value work is a few dense products with no chain over node
+// tiles.
+//
+// Theorem 1 (§4.1) with Lemma 2 for the delta rule, per (request, v-head):
+//   R = D_beta (V - D_P K S^T)                 R_j = beta_j (v_j - P_j S k_j)
+//   G_ij = beta_i 2^(cl_i - cl_j) (k_i . k_j)  for strict ancestors j of i
+//   U = (I + G)^{-1} R                         (Lemma 3: I + G is unit lower
+//                                              triangular in index order)
+//   O = q_scale (D_P Q S^T + C U)              C_ij = [j in Anc(i) u {i}]
+//                                                     2^(cl_i - cl_j) (q_i . k_j)
+// (stored orientation: S is the [d_v, d_k] slot; cl is the cumulative log2
+// decay along the root path.)
+//
+// The node-by-node coupling sits in A = (I + G)^{-1}, a T x T matrix that does
+// not depend on the value channels.  So one workgroup of 8 wave64s per
+// (request, v-head) runs three phases separated by two barriers:
+//  1. every wave forms its share of the 16 x 16 blocks (I, J <= I) of C and G
+//     (K_J Q_I^T and K_J K_I^T on MFMA, masked by the M+ rows, decayed) into
+//     LDS in MFMA operand order, then computes, for its own 16 value
+//     channels, B0 = Q S^T and SK = K S^T over all node tiles (state in bf16
+//     hi + lo) and R from SK;
+//  2. wave J solves column block J of A: for I = J, J + 1, ...,
+//       X_I = (I + G_II)^{-1} (delta_IJ - sum_{J <= K < I} G_IK X_K),
+//     the sum on MFMA, the in-tile part by forward substitution over the
+//     tile's in-tile ancestors (each step broadcasts a column of the tile
+//     along its 16-lane row by DPP).  Columns are independent, so the waves
+//     need no barrier between them.  A goes to LDS over the dead Q and K rows;
+//  3. every wave forms U = A R and O = q_scale (P B0 + C U) for its value
+//     channels: products of LDS operands (A, C) with register operands (R,
+//     U), no LDS round trip for the value side.
+// Blocks of C, G and A whose tile pair holds no ancestor relation are zero
+// and are neither formed nor read.  The matrices are fp32, split into bf16
+// hi + lo for the MFMA, with fp32 accumulation.
+#include <hip/hip_runtime.h>
+
+#include <utility>
+
+#include "tl_device.h"
+#include "tl_kernels.h"
+#include "verify_common.h"
+
+namespace tl {
+
+namespace {
+
+constexpr int kDenseWaves = 8;
+constexpr int kDenseThreads = 64 * kDenseWaves;
+constexpr int kDenseMaxTiles = 8;   // 128 nodes
+
+// MFMA 16x16x16 bf16: D = A (16 x 16) * B (16 x 16) + C.  Lane l supplies A
+// row (l % 16) and B column (l % 16), 4 values each of the K range owned by
+// lane group l / 16; D comes back as rows 4 (l / 16) .. + 3 of column l % 16.
+// So a D fragment is directly the B operand of a product whose K index is
+// D's row index.
+__device__ inline f32x4 mfma16k(const bf16x4& a, const bf16x4& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a),
+                                                   __builtin_bit_cast(s16x4, b), c, 0, 0, 0);
+}
+
+// f32x4 -> bf16x4 hi + lo (split2_bf16 on both pairs)
+__device__ inline void split4_bf16(const f32x4& x, bf16x4& hi, bf16x4& lo) {
+  uint32_t h0, h1, l0, l1;
+  split2_bf16(x[0], x[1], h0, l0);
+  split2_bf16(x[2], x[3], h1, l1);
+  hi = __builtin_bit_cast(bf16x4, uint2{h0, h1});
+  lo = __builtin_bit_cast(bf16x4, uint2{l0, l1});
+}
+
+__host__ __device__ constexpr int tri(int n) { return n * (n + 1) / 2; }
+
+// Blocks are stored in pairs of node tiles (J0, J0 + 1), J0 even, so that one
+// 16-byte read per lane yields a whole 16x16x32 operand: per lane
+// [hi of J0 | hi of J0 + 1 | lo of J0 | lo of J0 + 1], 32 bytes, 2 KB a pair.
+// Row I of a lower-triangular set (J <= I) holds I / 2 + 1 pairs (the half
+// J = I + 1 of an even row is kept zero); pair_row(I) is its first pair.
+// The strictly lower set of G (K < I) holds (I + 1) / 2 pairs a row.
+__host__ __device__ constexpr int pair_row(int I) { return (I / 2) * (I / 2 + 1) + ((I & 1) ? I / 2 + 1 : 0); }
+__host__ __device__ constexpr int gpair_row(int I) { return (I / 2) * (I / 2) + ((I & 1) ? I / 2 : 0); }
+
+template <class F, int... J>
+__device__ inline void static_for_seq(F& f, std::integer_sequence<int, J...>) {
+  (f(std::integral_constant<int, J>{}), ...);
+}
+template <int N, class F>
+__device__ inline void static_for(F& f) {
+  static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
+
+}  // namespace
+
+struct DenseLayout {
+  int cl, beta, mask, tmask, tin, gin, kq, cst, gst, xs, total;
+};
+
+// LDS layout (bytes); identical on host and device.
+__host__ __device__ inline DenseLayout dense_layout(int tm, int W) {
+  const int nb = tm / kTile;
+  DenseLayout L;
+  int o = 0;
+  L.cl = o;    o += align16((tm + 16) * 4);          // cumulative log2-decay
+  L.beta = o;  o += align16(tm * 4);
+  L.mask = o;  o += tm * W * 8;                      // M+ rows
+  L.tmask = o; o += align16(nb * W * 8);             // OR of M+ rows per node tile
+  L.tin = o;   o += align16(nb * 4);                 // in-tile strict ancestors per tile
+  L.gin = o;   o += nb * kTile * kTile * 4;          // in-tile blocks of G, row-major fp32
+  L.kq = o;                                          // K and Q rows | the blocks of A
+  {
+    const int rows = 2 * tm * 128 * 2, ablk = pair_row(nb) * 2048;
+    o += rows > ablk ? rows : ablk;
+  }
+  L.cst = o;                                         // blocks of C | topology scratch
+  {
+    const int cb = pair_row(nb) * 2048, topo = kThreads * (4 + 4 + 4) + kThreads * W * 8;
+    o += cb > topo ? cb : topo;
+  }
+  L.gst = o;   o += gpair_row(nb) * 2048;             // strictly lower blocks of -G
+  L.xs = o;    o += kDenseWaves * 1024;              // per-wave transposition buffer
+  L.total = o;
+  return L;
+}
+
+template <int W>
+__global__ __launch_bounds__(kDenseThreads) void verify_gdn_dense_kernel(VerifyArgs a) {
+  constexpr int D = 128;
+  constexpr int KS = D / 32;
+  constexpr int CPRK = D / 8;
+  constexpr int NTM = kDenseMaxTiles;
+  constexpr float kLog2e = 1.4426950408889634f;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63, lr = lane & 15, lg = lane >> 4;
+  lds_poison(a.lds_bytes);
+  TL_TRACE_POINT(a, 0);
+#ifdef TL_TRACE
+  if (a.trace && threadIdx.x == 0) a.trace[(size_t)blockIdx.x * 16 + 13] = (long long)__builtin_readcyclecounter();
+#endif
+
+  // ---- block -> (request, qk-head, v-head): grouped v-heads 8 ids apart (same XCD)
+  const int grp = a.Hv / a.Hk;
+  const int nshare = a.batch * a.Hk;
+  const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+  const int sh = (local / grp) * 8 + xcd;
+  if (sh >= nshare) return;
+  const int b = sh / a.Hk, hq = sh % a.Hk, h = hq * grp + local % grp;
+  Request rq;
+  if (!load_request(a.node_offsets, b, a.max_nodes, a.dev_err, rq)) return;
+  const int T = rq.T, off = rq.off;
+  if (T == 0) return;
+  const int sidx = a.slot ? a.slot[b] : b;
+  if (sidx < 0 || sidx >= a.num_slots) {
+    if (tid == 0) report(a.dev_err, TL_EINVAL);
+    return;
+  }
+  const int tm = a.tm;
+  const int nt = (T + kTile - 1) / kTile;   // node tiles of this tree (uniform)
+  const DenseLayout L = dense_layout(tm, W);
+  float* s_cl = reinterpret_cast<float*>(tl_lds + L.cl);
+  float* s_beta = reinterpret_cast<float*>(tl_lds + L.beta);
+  uint64_t* s_mask = reinterpret_cast<uint64_t*>(tl_lds + L.mask);
+  uint64_t* s_tmask = reinterpret_cast<uint64_t*>(tl_lds + L.tmask);
+  uint32_t* s_tin = reinterpret_cast<uint32_t*>(tl_lds + L.tin);
+  float* s_gin = reinterpret_cast<float*>(tl_lds + L.gin);
+  __bf16* s_k = reinterpret_cast<__bf16*>(tl_lds + L.kq);
+  __bf16* s_q = s_k + tm * D;
+  unsigned char* s_a = tl_lds + L.kq;      // blocks of A, over the dead K and Q rows
+  unsigned char* s_c = tl_lds + L.cst;
+  unsigned char* s_g = tl_lds + L.gst;
+  unsigned char* s_xs = tl_lds + L.xs + wave * 1024;
+
+  const size_t qk_row = (size_t)a.Hk * D, v_row = (size_t)a.Hv * D;
+  const __bf16* Qb = reinterpret_cast<const __bf16*>(a.q) + (size_t)off * qk_row + (size_t)hq * D;
+  const __bf16* Kb = reinterpret_cast<const __bf16*>(a.k) + (size_t)off * qk_row + (size_t)hq * D;
+  const __bf16* Vb = reinterpret_cast<const __bf16*>(a.v) + (size_t)off * v_row + (size_t)h * D;
+
+  // ---- prologue.  Loads in the order they are needed: parents and gates,
+  // K and Q rows (direct copies into swizzled LDS), the V values of the
+  // wave's channels, then the wave's state rows (needed last, in phase 1b).
+  TL_TRACE_POINT(a, 1);
+  int par = -1;
+  float gx = 0.f, bx = 0.f;
+  if (tid < T) {
+    par = a.parent[off + tid];
+    gx = a.g[(size_t)(off + tid) * a.Hv + h];
+    bx = a.beta[(size_t)(off + tid) * a.Hv + h];
+  }
+  for (int base = wave * 64; base < T * CPRK; base += kDenseThreads) {
+    const int p = base + lane;
+    if (p < T * CPRK) {
+      const int r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
+      copy16_to_lds_async(Kb + (size_t)r * qk_row + c * 8, s_k + (size_t)base * 8);
+      copy16_to_lds_async(Qb + (size_t)r * qk_row + c * 8, s_q + (size_t)base * 8);
+    }
+  }
+  // V[node 16 J + 4 lg + e][channel 16 wave + lr], rows clamped to the tree
+  bf16x4 vv[NTM];
+#pragma unroll
+  for (int J = 0; J < NTM; ++J) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = min(kTile * J + 4 * lg + e, T - 1);
+      vv[J][e] = Vb[(size_t)r * v_row + kTile * wave + lr];
+    }
+  }
+  TL_TRACE_POINT(a, 6);
+  // S^T as the B operand of 16x16x32 products: column = channel 16 wave + lr
+  // (a row of the stored slot), K = the key channels of chunk ks in kpos order
+  f32x4 sraw[KS][2];
+  {
+    const float* row = a.state + ((size_t)sidx * a.Hv + h) * D * D + (size_t)(kTile * wave + lr) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      sraw[ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 4 * lg));
+      sraw[ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 16 + 4 * lg));
+    }
+  }
+
+  // ---- topology: M+ rows, cumulative log-decay, per-tile masks
+  TL_TRACE_POINT(a, 2);
+  for (int x = tid; x < (tm / kTile) * W; x += kDenseThreads) s_tmask[x] = 0;
+  for (int x = tid; x < tm / kTile; x += kDenseThreads) s_tin[x] = 0u;
+  {
+    int* s_jmp = reinterpret_cast<int*>(s_c);
+    float* s_acc = reinterpret_cast<float*>(s_jmp + kThreads);
+    int* s_cnt = reinterpret_cast<int*>(s_acc + kThreads);
+    uint64_t* s_msk = reinterpret_cast<uint64_t*>(s_cnt + kThreads);
+    int dep = 0;
+    float cl = 0.f;
+    uint64_t msk[W];
+    const bool ok = build_topology<W, true>(par, T, gx, s_jmp, s_acc, s_cnt, s_msk, dep, cl, msk);
+    if (!ok) {
+      if (tid == 0) report(a.dev_err, TL_EBADTREE);
+      wait_vmem();   // let the in-flight LDS copies land before the block retires
+      return;
+    }
+    __syncthreads();   // topology scratch is dead from here
+    if (tid < T) {
+      s_cl[tid] = cl * kLog2e;
+      s_beta[tid] = bx;
+      const int I = tid / kTile;
+#pragma unroll
+      for (int w = 0; w < W; ++w) {
+        s_mask[tid * W + w] = msk[w];
+        if (msk[w]) atomicOr(reinterpret_cast<unsigned long long*>(&s_tmask[I * W + w]),
+                             (unsigned long long)msk[w]);
+      }
+      uint64_t wv = msk[0];
+#pragma unroll
+      for (int w = 1; w < W; ++w)
+        if ((tid >> 6) == w) wv = msk[w];
+      const uint32_t in_tile = (uint32_t)(wv >> ((I & 3) * kTile)) & 0xFFFFu & ~(1u << (tid & 15));
+      if (in_tile) atomicOr(&s_tin[I], in_tile);
+    }
+  }
+  TL_TRACE_POINT(a, 7);
+  // the K and Q copies (issued first) have landed once at most the V and
+  // state loads of this wave are outstanding
+  wait_vmem_below<4 * NTM + 2 * KS>();
+  lds_barrier();   // K, Q, masks and decays are in LDS (V and the state stay in flight)
+  TL_TRACE_POINT(a, 3);
+
+  // operand fragment of row R + lr of the swizzled K or Q rows (R a multiple of 16)
+  const int key = lr & (CPRK - 1);
+  const int fo_row = lr * D * 2 + (lg & 1) * 8;
+  auto frag = [&](const __bf16* base, int R, int ks) __attribute__((always_inline)) {
+    const unsigned char* p = reinterpret_cast<const unsigned char*>(base) + R * D * 2 + fo_row;
+    const bf16x4 x0 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + (lg >> 1)) ^ key) * 16));
+    const bf16x4 x1 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + 2 + (lg >> 1)) ^ key) * 16));
+    return bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+  };
+  // block x (fp32, MFMA fragment layout) into half `half` of pair `pair`
+  auto put_half = [&](unsigned char* base, int pair, int half, const f32x4& x) __attribute__((always_inline)) {
+    bf16x4 hi, lo;
+    split4_bf16(x, hi, lo);
+    unsigned char* q = base + pair * 2048 + lane * 32 + half * 8;
+    *reinterpret_cast<bf16x4*>(q) = hi;
+    *reinterpret_cast<bf16x4*>(q + 16) = lo;
+  };
+  auto zero_half = [&](unsigned char* base, int pair, int half) __attribute__((always_inline)) {
+    unsigned char* q = base + pair * 2048 + lane * 32 + half * 8;
+    *reinterpret_cast<uint2*>(q) = uint2{0u, 0u};
+    *reinterpret_cast<uint2*>(q + 16) = uint2{0u, 0u};
+  };
+  auto get_pair = [&](const unsigned char* base, int pair, bf16x8& hi, bf16x8& lo) __attribute__((always_inline)) {
+    const unsigned char* q = base + pair * 2048 + lane * 32;
+    hi = *reinterpret_cast<const bf16x8*>(q);
+    lo = *reinterpret_cast<const bf16x8*>(q + 16);
+  };
+  // fp32 fragment x -> half `half` of a register pair operand (hi, lo)
+  // (`half` is a compile-time constant wherever this is used)
+  auto set_half = [&](bf16x8& hi, bf16x8& lo, int half, const f32x4& x) __attribute__((always_inline)) {
+    bf16x4 h, l;
+    split4_bf16(x, h, l);
+    if (half == 0) {
+      hi = bf16x8{h[0], h[1], h[2], h[3], hi[4], hi[5], hi[6], hi[7]};
+      lo = bf16x8{l[0], l[1], l[2], l[3], lo[4], lo[5], lo[6], lo[7]};
+    } else {
+      hi = bf16x8{hi[0], hi[1], hi[2], hi[3], h[0], h[1], h[2], h[3]};
+      lo = bf16x8{lo[0], lo[1], lo[2], lo[3], l[0], l[1], l[2], l[3]};
+    }
+  };
+
+  // tile pairs (I, J <= I) that hold an ancestor relation, as one uniform
+  // 64-bit mask (bit 8 I + J); other blocks of C, G and A are zero
+  uint64_t live_bits;
+  {
+    const int I = lane >> 3, J = lane & 7;   // lane 8 I + J tests tile pair (I, J)
+    const uint64_t m = s_tmask[min(I, tm / kTile - 1) * W + min(J >> 2, W - 1)];
+    live_bits = __ballot(J <= I && I < nt && ((m >> ((J & 3) * kTile)) & 0xFFFFull) != 0ull);
+  }
+  auto live = [&](int I, int J) __attribute__((always_inline)) { return (live_bits >> (8 * I + J)) & 1ull; };
+
+  // ---- 1a. blocks (I, J <= I) of C and G, dealt out round robin over the
+  // waves, every block formed (the masks zero the dead ones, so later phases
+  // read them without tests).  K_J Q_I^T comes back with column
+  // i = 16 I + lr and rows j = 16 J + 4 lg + r: per lane exactly the
+  // A-operand elements of C_IJ in C U (row i, K = nodes j), and likewise
+  // K_J K_I^T gives the B-operand elements of G_IJ^T.
+  const int nblk = tri(nt);
+  // block k -> (I, J), J <= I, without a loop (k < 36)
+  auto row_of = [](int k) __attribute__((always_inline)) {
+    return (k >= 1) + (k >= 3) + (k >= 6) + (k >= 10) + (k >= 15) + (k >= 21) + (k >= 28);
+  };
+  auto form = [&](int k, f32x4& cv, f32x4& gv) __attribute__((always_inline)) {
+    const int I = row_of(k), J = k - tri(I);
+    const int i = kTile * I + lr;
+    const bool iv = i < T;
+    f32x4 qk = f32x4{0.f, 0.f, 0.f, 0.f}, kk = qk;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 kj = frag(s_k, kTile * J, ks);
+      qk = mfma16(kj, frag(s_q, kTile * I, ks), qk);
+      kk = mfma16(kj, frag(s_k, kTile * I, ks), kk);
+    }
+    // loads clamped into the arrays and the values selected, so that no
+    // LDS read sits under a branch
+    const uint64_t mw0 = s_mask[min(i, tm - 1) * W + (J >> 2)];
+    const float cl0 = s_cl[i], b00 = s_beta[min(i, tm - 1)];
+    const uint64_t mw = iv ? mw0 : 0ull;
+    const unsigned mb = (unsigned)(mw >> ((J & 3) * kTile + 4 * lg)) & 0xFu;
+    const float cli = iv ? cl0 : 0.f, bi = iv ? b00 : 0.f;
+    const f32x4 clj = *reinterpret_cast<const f32x4*>(s_cl + kTile * J + 4 * lg);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const bool m = (mb >> r) & 1u;
+      const bool self = J == I && 4 * lg + r == lr;
+      const float dec = __builtin_amdgcn_exp2f(cli - clj[r]);
+      const float c = (dec * a.q_scale) * qk[r], g = (bi * dec) * kk[r];
+      cv[r] = m ? c : 0.f;
+      gv[r] = (m && !self) ? g : 0.f;
+    }
+  };
+  auto store = [&](int k, const f32x4& cv, const f32x4& gv) __attribute__((always_inline)) {
+    const int I = row_of(k), J = k - tri(I);
+    put_half(s_c, pair_row(I) + J / 2, J & 1, cv);
+    if (J < I) {
+      put_half(s_g, gpair_row(I) + J / 2, J & 1, -gv);   // stored negated: products accumulate -G
+    } else {
+      *reinterpret_cast<f32x4*>(s_gin + I * kTile * kTile + lr * kTile + 4 * lg) = gv;
+      // the halves no block fills: (I, I + 1) of C for even I, (I, I) of G for odd I
+      if ((I & 1) == 0) zero_half(s_c, pair_row(I) + I / 2, 1);
+      else zero_half(s_g, gpair_row(I) + I / 2, 1);
+    }
+  };
+  // two blocks per step: independent MFMA chains in flight together (the
+  // block coordinates come without a loop, so both sit in one basic block)
+  for (int k = wave; k < nblk; k += 2 * kDenseWaves) {   // uniform
+    const int k2 = k + kDenseWaves;
+    f32x4 c0, g0, c1, g1;
+    form(k, c0, g0);
+    form(min(k2, nblk - 1), c1, g1);
+    store(k, c0, g0);
+    if (k2 < nblk) store(k2, c1, g1);
+  }
+  TL_TRACE_POINT(a, 8);
+
+  // ---- 1b. B0 = Q S^T and SK = K S^T for this wave's channels, all node tiles
+  // (rows = nodes 16 I + 4 lg + r, column = channel 16 wave + lr)
+  bf16x8 shi[KS], slo[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) split8_bf16(sraw[ks][0], sraw[ks][1], shi[ks], slo[ks]);
+  f32x4 b0[NTM];
+  bf16x8 rph[NTM / 2], rpl[NTM / 2];   // R as B operands, tiles paired (K = nodes of 2 P, 2 P + 1)
+#pragma unroll
+  for (int P = 0; P < NTM / 2; ++P) {
+    rph[P] = bf16x8{};
+    rpl[P] = bf16x8{};
+  }
+#pragma unroll
+  for (int I = 0; I < NTM; ++I) {
+    b0[I] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (I < nt) {   // uniform
+      f32x4 sk = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 qf = frag(s_q, kTile * I, ks), kf = frag(s_k, kTile * I, ks);
+        b0[I] = mfma16(qf, shi[ks], b0[I]);
+        sk = mfma16(kf, shi[ks], sk);
+        b0[I] = mfma16(qf, slo[ks], b0[I]);
+        sk = mfma16(kf, slo[ks], sk);
+      }
+      // R_j = beta_j (v_j - P_j (S k_j)); zero past the tree (those columns of
+      // A meet only zero coefficients, and must stay finite)
+      const f32x4 clj = *reinterpret_cast<const f32x4*>(s_cl + kTile * I + 4 * lg);
+      const f32x4 bj = *reinterpret_cast<const f32x4*>(s_beta + kTile * I + 4 * lg);
+      f32x4 rv;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool jv = kTile * I + 4 * lg + r < T;
+        rv[r] = jv ? bj[r] * ((float)vv[I][r] - __builtin_amdgcn_exp2f(clj[r]) * sk[r]) : 0.f;
+      }
+      set_half(rph[I / 2], rpl[I / 2], I & 1, rv);
+    }
+  }
+  lds_barrier();   // C, G and the in-tile blocks are in LDS; K and Q are dead
+  TL_TRACE_POINT(a, 4);
+
+  // ---- 2. column block J = wave of A = (I + G)^{-1}.  X^T_I (rows: columns
+  // 16 J + 4 lg + r of A; column: node i = 16 I + lr) is in MFMA output
+  // layout, which is per lane the A-operand element of A_IJ in U = A R.
+  // Every block (I, J <= I) of A is written, zero where no ancestor relation.
+  if (wave < nt) {   // uniform
+    const int J = wave;
+    bf16x8 xph[NTM / 2], xpl[NTM / 2];   // X^T_K as A operands, tiles paired (zero below J)
+#pragma unroll
+    for (int P = 0; P < NTM / 2; ++P) {
+      xph[P] = bf16x8{};
+      xpl[P] = bf16x8{};
+    }
+    auto step_tile = [&](auto Ic) __attribute__((always_inline)) {
+      constexpr int I = decltype(Ic)::value;
+      if (I < J || I >= nt) return;   // uniform
+      const int pa = pair_row(I) + J / 2;
+      if (I == J && (I & 1) == 0) zero_half(s_a, pa, 1);   // (I, I + 1): never a block
+      if (!live(I, J)) {              // A_IJ = 0
+        zero_half(s_a, pa, J & 1);
+        return;
+      }
+      // this lane's row of the in-tile block of G (node i = 16 I + lr)
+      const float* gi = s_gin + I * kTile * kTile + lr * kTile;
+      const f32x4 g0 = *reinterpret_cast<const f32x4*>(gi), g1 = *reinterpret_cast<const f32x4*>(gi + 4),
+                  g2 = *reinterpret_cast<const f32x4*>(gi + 8), g3 = *reinterpret_cast<const f32x4*>(gi + 12);
+      const unsigned tin = __builtin_amdgcn_readfirstlane(s_tin[I]);
+      f32x4 y, y2 = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) y[r] = (I == J && 4 * lg + r == lr) ? 1.f : 0.f;
+      // - sum_{K < I} X^T_K G_IK^T over tile pairs (X^T_K is zero below J and
+      // where A_KJ is; the half K = I of the last pair is zero), G stored negated
+#pragma unroll
+      for (int P = 0; 2 * P < I; ++P) {
+        if (2 * P + 1 < J) continue;   // uniform: both halves of X^T are zero
+        bf16x8 gh, gl;
+        get_pair(s_g, gpair_row(I) + P, gh, gl);
+        y = mfma16(xph[P], gh, y);
+        y2 = mfma16(xph[P], gl, y2);
+        y = mfma16(xpl[P], gh, y);
+      }
+      y += y2;
+      // in-tile forward substitution: x_i -= G_is x_s over the in-tile
+      // strict ancestors s of i, in index order (lane s of each 16-lane row
+      // holds x_s and broadcasts it by DPP row_newbcast)
+      auto sub = [&](auto sc) __attribute__((always_inline)) {
+        constexpr int s = decltype(sc)::value;
+        if ((tin >> s) & 1u) {   // uniform
+          const float gis = s < 4 ? g0[s & 3] : s < 8 ? g1[s & 3] : s < 12 ? g2[s & 3] : g3[s & 3];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float xs = __int_as_float(
+                __builtin_amdgcn_mov_dpp(__float_as_int(y[r]), 0x150 + s, 0xF, 0xF, false));
+            y[r] -= gis * xs;
+          }
+        }
+      };
+      static_for<kTile>(sub);
+      // A_IJ for phase 3
+      put_half(s_a, pa, J & 1, y);
+      // X^T_I as an A operand for the later tiles: element (row 4 lg + r,
+      // column lr) goes to lane (4 lg + r) + 16 (lr / 4), slot lr % 4
+      if (I + 1 < nt) {
+        bf16x4 hi, lo;
+        split4_bf16(y, hi, lo);
+        unsigned char* xs = s_xs;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 4 * lg + r + 16 * (lr >> 2);
+          *reinterpret_cast<__bf16*>(xs + t * 8 + (lr & 3) * 2) = hi[r];
+          *reinterpret_cast<__bf16*>(xs + 512 + t * 8 + (lr & 3) * 2) = lo[r];
+        }
+        const bf16x4 th = *reinterpret_cast<const bf16x4*>(xs + lane * 8);
+        const bf16x4 tl = *reinterpret_cast<const bf16x4*>(xs + 512 + lane * 8);
+        if constexpr ((I & 1) == 0) {
+          xph[I / 2] = bf16x8{th[0], th[1], th[2], th[3], xph[I / 2][4], xph[I / 2][5], xph[I / 2][6], xph[I / 2][7]};
+          xpl[I / 2] = bf16x8{tl[0], tl[1], tl[2], tl[3], xpl[I / 2][4], xpl[I / 2][5], xpl[I / 2][6], xpl[I / 2][7]};
+        } else {
+          xph[I / 2] = bf16x8{xph[I / 2][0], xph[I / 2][1], xph[I / 2][2], xph[I / 2][3], th[0], th[1], th[2], th[3]};
+          xpl[I / 2] = bf16x8{xpl[I / 2][0], xpl[I / 2][1], xpl[I / 2][2], xpl[I / 2][3], tl[0], tl[1], tl[2], tl[3]};
+        }
+      }
+    };
+    static_for<NTM>(step_tile);
+  }
+  lds_barrier();   // A is in LDS
+  TL_TRACE_POINT(a, 5);
+
+  // ---- 3. U = A R, then O = q_scale (P B0 + C U), for this wave's channels:
+  // 16x16x32 products over pairs of node tiles, both operands read whole
+  bf16x8 uph[NTM / 2], upl[NTM / 2];
+#pragma unroll
+  for (int P = 0; P < NTM / 2; ++P) {
+    uph[P] = bf16x8{};
+    upl[P] = bf16x8{};
+  }
+  auto pair_live = [&](int I, int P) __attribute__((always_inline)) {
+    return live(I, 2 * P) || (2 * P + 1 <= I && live(I, 2 * P + 1));
+  };
+#pragma unroll
+  for (int I = 0; I < NTM; ++I) {
+    if (I >= nt) break;   // uniform
+    f32x4 u = f32x4{0.f, 0.f, 0.f, 0.f}, u2 = u;
+#pragma unroll
+    for (int P = 0; 2 * P <= I; ++P) {
+      if (!pair_live(I, P)) continue;   // uniform
+      bf16x8 ah, al;
+      get_pair(s_a, pair_row(I) + P, ah, al);
+      u = mfma16(ah, rph[P], u);
+      u2 = mfma16(ah, rpl[P], u2);
+      u = mfma16(al, rph[P], u);
+    }
+    set_half(uph[I / 2], upl[I / 2], I & 1, u + u2);
+  }
+  float* obase = a.out + (size_t)(off + 4 * lg) * v_row + (size_t)h * D + kTile * wave + lr;
+#pragma unroll
+  for (int I = 0; I < NTM; ++I) {
+    if (I >= nt) break;   // uniform
+    f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f}, o2 = o;
+#pragma unroll
+    for (int P = 0; 2 * P <= I; ++P) {
+      if (!pair_live(I, P)) continue;   // uniform
+      bf16x8 ch, cl;
+      get_pair(s_c, pair_row(I) + P, ch, cl);
+      o = mfma16(ch, uph[P], o);
+      o2 = mfma16(ch, upl[P], o2);
+      o = mfma16(cl, uph[P], o);
+    }
+    const f32x4 cli = *reinterpret_cast<const f32x4*>(s_cl + kTile * I + 4 * lg);
+    float* orow = obase + (size_t)(kTile * I) * v_row;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float v = a.q_scale * __builtin_amdgcn_exp2f(cli[r]) * b0[I][r] + (o[r] + o2[r]);
+      if (kTile * I + 4 * lg + r < T) __builtin_nontemporal_store(v, orow + (size_t)r * v_row);
+    }
+  }
+  TL_TRACE_POINT(a, 15);
+#ifdef TL_TRACE
+  if (a.trace && threadIdx.x == 0) a.trace[(size_t)blockIdx.x * 16 + 14] = (long long)__builtin_readcyclecounter();
+#endif
+}
+
+int verify_gdn_dense_lds_bytes(int tm) { return dense_layout(tm, tm > 64 ? 2 : 1).total; }
+
+template <int W>
+static tl_status launch_dense_w(const VerifyArgs& a, hipStream_t stream) {
+  const int lds = dense_layout(a.tm, W).total;
+  if (lds > 160 * 1024) return TL_EUNSUPPORTED;
+  const long blocks = 8 * (((long)a.batch * a.Hk + 7) / 8) * (a.Hv / a.Hk);
+  if (blocks == 0) return TL_OK;
+  if (blocks > 0x7fffffffL) return TL_EINVAL;
+  auto kern = verify_gdn_dense_kernel<W>;
+  if (lds > 64 * 1024) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess)
+      return TL_EHIP;
+  }
+  VerifyArgs b = a;
+  b.lds_bytes = lds;
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kDenseThreads), lds, stream, b);
+  return hipGetLastError() == hipSuccess ? TL_OK : TL_EHIP;
+}
+
+tl_status launch_verify_gdn_dense(const tl_problem& p, const VerifyArgs& a, hipStream_t stream) {
+  if (p.mode != TL_MODE_GDN || p.in_dtype != TL_BF16 || p.d_k != 128 || a.tm > 128)
+    return TL_EUNSUPPORTED;
+  return a.tm > 64 ? launch_dense_w<2>(a, stream) : launch_dense_w<1>(a, stream);
+}
+
+}  // namespace tl
