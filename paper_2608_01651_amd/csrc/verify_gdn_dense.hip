@@ -71,8 +71,10 @@ __device__ inline void split4_bf16(const f32x4& x, bf16x4& hi, bf16x4& lo) {
 __host__ __device__ constexpr int tri(int n) { return n * (n + 1) / 2; }
 
 // Blocks are stored in pairs of node tiles (J0, J0 + 1), J0 even, so that one
-// 16-byte read per lane yields a whole 16x16x32 operand: per lane
-// [hi of J0 | hi of J0 + 1 | lo of J0 | lo of J0 + 1], 32 bytes, 2 KB a pair.
+// 16-byte read per lane yields a whole 16x16x32 operand: a 1 KB plane of
+// hi parts, [lane][hi of J0 | hi of J0 + 1], then one of lo parts, 2 KB a
+// pair (16 bytes per lane per plane, so the reads are free of bank
+// conflicts).
 // Row I of a lower-triangular set (J <= I) holds I / 2 + 1 pairs (the half
 // J = I + 1 of an even row is kept zero); pair_row(I) is its first pair.
 // The strictly lower set of G (K < I) holds (I + 1) / 2 pairs a row.
@@ -273,19 +275,19 @@ __global__ __launch_bounds__(kDenseThreads) void verify_gdn_dense_kernel(VerifyA
   auto put_half = [&](unsigned char* base, int pair, int half, const f32x4& x) __attribute__((always_inline)) {
     bf16x4 hi, lo;
     split4_bf16(x, hi, lo);
-    unsigned char* q = base + pair * 2048 + lane * 32 + half * 8;
+    unsigned char* q = base + pair * 2048 + lane * 16 + half * 8;
     *reinterpret_cast<bf16x4*>(q) = hi;
-    *reinterpret_cast<bf16x4*>(q + 16) = lo;
+    *reinterpret_cast<bf16x4*>(q + 1024) = lo;
   };
   auto zero_half = [&](unsigned char* base, int pair, int half) __attribute__((always_inline)) {
-    unsigned char* q = base + pair * 2048 + lane * 32 + half * 8;
+    unsigned char* q = base + pair * 2048 + lane * 16 + half * 8;
     *reinterpret_cast<uint2*>(q) = uint2{0u, 0u};
-    *reinterpret_cast<uint2*>(q + 16) = uint2{0u, 0u};
+    *reinterpret_cast<uint2*>(q + 1024) = uint2{0u, 0u};
   };
   auto get_pair = [&](const unsigned char* base, int pair, bf16x8& hi, bf16x8& lo) __attribute__((always_inline)) {
-    const unsigned char* q = base + pair * 2048 + lane * 32;
+    const unsigned char* q = base + pair * 2048 + lane * 16;
     hi = *reinterpret_cast<const bf16x8*>(q);
-    lo = *reinterpret_cast<const bf16x8*>(q + 16);
+    lo = *reinterpret_cast<const bf16x8*>(q + 1024);
   };
   // fp32 fragment x -> half `half` of a register pair operand (hi, lo)
   // (`half` is a compile-time constant wherever this is used)
