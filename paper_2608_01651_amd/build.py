@@ -28,7 +28,7 @@ LIB_DEBUG = os.path.join(PKG, "libtreelin_debug.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["verify.hip", "verify_tiled.hip", "verify_gdn_dense.hip", "commit.hip", "topology.hip", "conv.hip", "budget.hip",
+SOURCES = ["verify.hip", "verify_tiled.hip", "verify_gla_large.hip", "verify_gdn_dense.hip", "commit.hip", "topology.hip", "conv.hip", "budget.hip",
            "abi.cpp"]
 COMMON = ["-std=c++17", "-O3", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}",
           "-Wall", "-Wno-unused-function"]

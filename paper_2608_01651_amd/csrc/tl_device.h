@@ -9,12 +9,15 @@
 #include "treelin.h"
 
 // Phase time stamps for trace builds (-DTL_TRACE): thread 0 of each block
-// records the 100 MHz wall clock at point k.  Empty in normal builds.
+// records the 100 MHz wall clock at point k (and, at point 0, its compute unit
+// id in slot 12).  Empty in normal builds.
 #ifdef TL_TRACE
 #define TL_TRACE_POINT(args, k)                                                           \
   do {                                                                                    \
-    if ((args).trace && threadIdx.x == 0)                                                 \
+    if ((args).trace && threadIdx.x == 0) {                                               \
       (args).trace[(size_t)blockIdx.x * 16 + (k)] = wall_clock64();                       \
+      if ((k) == 0) (args).trace[(size_t)blockIdx.x * 16 + 12] = __smid();                \
+    }                                                                                     \
   } while (0)
 #else
 #define TL_TRACE_POINT(args, k) \

@@ -10,10 +10,10 @@
 //               jumping: gated linear attention over node caps of <= 64
 //               (bf16, d >= 32), the small-tree MFMA kernel;
 //   kTopoLds    build_topology<W>, LDS pointer jumping over one thread per
-//               node: the tile-walk kernel (gated linear attention over
-//               larger caps, the delta rule where its layout fits LDS), and
-//               the vector path (fp32 inputs or d = 16), whose own pass
-//               counts depths without masks;
+//               node: the large-tree kernel of gated linear attention (caps
+//               of 65..256), the delta rule's tile walk (where its layout
+//               fits LDS), and the vector path (fp32 inputs or d = 16), whose
+//               own pass counts depths without masks;
 //   kTopoGdn    the delta rule's kernel for node caps beyond the tile walk's
 //               LDS (d = 128, caps of 176..256): wave_topology for trees of
 //               <= 64 nodes, build_topology<4> above.

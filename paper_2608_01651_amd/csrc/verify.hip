@@ -181,13 +181,13 @@ tl_status launch_verify(const tl_problem& p, const VerifyArgs& a, hipStream_t st
   if (p.mode == TL_MODE_GDN && p.in_dtype == TL_BF16 && p.d_k == 128 && a.tm <= 128)
     return launch_verify_gdn_dense(p, a, stream);
   // bf16 inputs, d >= 32: gated linear attention over trees of more than 64
-  // nodes, and the delta rule wherever its tile-sequential layout fits in
-  // LDS (node caps of up to 160 at d = 128), run node tile by node tile
-  // (verify_tiled.hip)
+  // nodes, node tile by node tile with every operand resident on chip
+  // (verify_gla_large.hip); the delta rule wherever its tile-sequential
+  // layout fits in LDS (node caps of up to 160 at d = 128, verify_tiled.hip)
   if (p.in_dtype == TL_BF16 && p.d_k >= 32) {
+    if (p.mode == TL_MODE_GLA && a.tm > 64) return launch_verify_gla_large(p, a, stream);
     const int W = a.tm > 128 ? 4 : (a.tm > 64 ? 2 : 1);
-    if (p.mode == TL_MODE_GLA ? a.tm > 64
-                              : verify_tiled_lds_bytes(p.mode, p.d_k, a.tm, W) <= 160 * 1024)
+    if (p.mode == TL_MODE_GDN && verify_tiled_lds_bytes(p.mode, p.d_k, a.tm, W) <= 160 * 1024)
       return launch_verify_tiled(p, a, stream);
   }
   if (p.mode == TL_MODE_GLA)

@@ -1,0 +1,422 @@
+// Verify, gated linear attention on MFMA over trees of 65..256 nodes.
+//
+// One workgroup per (request, v-head), one wave per 16-row value tile of the
+// stored state (8 waves at d = 128; at d < 128 spare waves only help form
+// coefficients).  Theorem 1 with U = V (§4.1):
+//   O^T = q_scale P .* (S Q^T) + V^T C^T,
+//   C_ij = [j in Anc(i) u {i}] 2^(cl_i - cl_j) (q_i . k_j) q_scale,
+// with cl the cumulative log2-decay along the root path.  Nodes are taken in
+// tiles of 16 in index order, which is topological, so the ancestors of tile
+// I lie in tiles 0..I.
+//
+// Everything the node tiles read is made resident on chip before the first
+// tile, so the tile walk issues no global load: its only global accesses are
+// the output stores.  (Loads and stores share one completion counter on this
+// GPU, and the compiler waits for every outstanding access wherever a loaded
+// register is first read while a store is pending; a walk that read
+// prefetched rows waited for the previous tile's stores at every tile.)
+//
+//  prologue  batch 1: parents and gates (thread = node), the wave's state
+//            rows (registers), and, by direct global -> LDS copies, the V rows
+//            (into the K region; rows past T repeat row T - 1) and the Q rows.
+//            Each value wave then reads its V^T operand fragments of every
+//            32-node chunk out of the staged rows with LDS transpose reads
+//            (ds_read_b64_tr_b16; 32 VGPRs at 256 nodes), entries of nodes
+//            >= T set to zero.  Batch 2 copies the K rows over the staged V
+//            rows while the topology is built (M+ rows, cl, per-tile OR of the
+//            M+ rows; LDS pointer jumping, whose barriers wait for LDS only).
+//  tile I    (a) coefficients: the ancestor columns of a tile are cut into
+//            chunks of 32 nodes (tiles 2c, 2c + 1) and dealt out to the waves
+//            by half chunk (one 16-node tile J).  A half chunk is one K_J
+//            Q_I^T MFMA chain; its output lanes hold B-operand elements of
+//            V^T C^T, so it is masked, decayed, split into bf16 hi + lo and
+//            stored in operand order.  Half chunks without an ancestor of the
+//            tile (tile masks) are stored as zeros without MFMA work.
+//            (b) per value wave: S Q_I^T with the state split into bf16
+//            hi + lo (two MFMA chains), plus V^T C^T over the chunks that hold
+//            an ancestor (two chains, hi and lo), scaled, added and stored.
+//  When LDS holds two chunk buffers, (a) of tile I + 1 and (b) of tile I share
+//  one step and one barrier; otherwise (node caps of 240 and 256 at d = 128)
+//  they alternate between two barriers.
+#include <hip/hip_runtime.h>
+
+#include "tl_device.h"
+#include "tl_kernels.h"
+#include "verify_common.h"
+
+namespace tl {
+
+__host__ __device__ constexpr int gla_large_waves(int D) { return D / kTile > kWaves ? D / kTile : kWaves; }
+
+// Rows of the K region: the K rows of tm nodes, and before them the V rows of
+// every 32-node chunk a tree of tm nodes reads.
+__host__ __device__ constexpr int gla_large_rows(int tm) { return (tm + 31) & ~31; }
+
+struct GlaLargeLayout {
+  int cl, mask, tmask, kst, qst, frag, fragsz, frag2, total;
+};
+
+// LDS layout (bytes); identical on host and device.  With db the chunk
+// operands are double-buffered.
+__host__ __device__ inline GlaLargeLayout gla_large_layout(int D, int tm, int W, bool db) {
+  GlaLargeLayout L;
+  int o = 0;
+  L.cl = o;    o += align16(tm * 4);                     // cumulative log2-decay (0 past T)
+  L.mask = o;  o += tm * W * 8;                          // M+ rows (0 past T)
+  L.tmask = o; o += align16((tm / kTile) * W * 8);       // OR of the M+ rows per node tile
+  L.kst = o;   o += gla_large_rows(tm) * D * 2;          // K rows | staged V rows, swizzled bf16
+  L.qst = o;   o += tm * D * 2;                          // Q rows, swizzled bf16
+  L.frag = o;                                            // chunk operands | topology scratch
+  L.fragsz = ((tm + 31) / 32) * 2 * 1024;                // chunks of tiles 0..I: C hi, C lo
+  const int topo = kThreads * (4 + 4 + 4) + kThreads * W * 8;
+  const int fr = (db ? 2 : 1) * L.fragsz;
+  o += align16(fr > topo ? fr : topo);
+  L.frag2 = db ? L.frag + L.fragsz : L.frag;
+  L.total = o;
+  return L;
+}
+
+template <int D, int W, bool DB>
+__global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kernel(VerifyArgs a) {
+  constexpr int NW = gla_large_waves(D);
+  constexpr int NT = 64 * NW;
+  constexpr int VT = D / kTile;            // value tiles: wave w < VT owns rows 16w..16w+15
+  constexpr int KS = D / 32;
+  constexpr int CPRK = D / 8;              // 16-byte chunks per row
+  constexpr int NCH = 2 * W;               // 32-node chunks of the largest tree
+  constexpr float kLog2e = 1.4426950408889634f;
+  static_assert(NT >= 64 * W, "one thread per node in the topology");
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63, lr = lane & 15, lg = lane >> 4;
+  const bool vw = wave < VT;
+  lds_poison(a.lds_bytes);
+  TL_TRACE_POINT(a, 0);
+
+  // ---- block -> (request, qk-head, v-head): the grouped v-heads of a qk-head
+  // get ids 8 apart (same XCD, shared L2 for q/k)
+  const int grp = a.Hv / a.Hk;
+  const int nshare = a.batch * a.Hk;
+  const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+  const int sh = (local / grp) * 8 + xcd;
+  if (sh >= nshare) return;
+  const int b = sh / a.Hk, hq = sh % a.Hk, h = hq * grp + local % grp;
+  Request rq;
+  if (!load_request(a.node_offsets, b, a.max_nodes, a.dev_err, rq)) return;
+  const int T = rq.T, off = rq.off;
+  if (T == 0) return;
+  const int sidx = a.slot ? a.slot[b] : b;
+  if (sidx < 0 || sidx >= a.num_slots) {
+    if (tid == 0) report(a.dev_err, TL_EINVAL);
+    return;
+  }
+  const int tm = a.tm;
+  const GlaLargeLayout L = gla_large_layout(D, tm, W, DB);
+  float* s_cl = reinterpret_cast<float*>(tl_lds + L.cl);
+  uint64_t* s_mask = reinterpret_cast<uint64_t*>(tl_lds + L.mask);
+  uint64_t* s_tmask = reinterpret_cast<uint64_t*>(tl_lds + L.tmask);
+  __bf16* s_k = reinterpret_cast<__bf16*>(tl_lds + L.kst);
+  __bf16* s_q = reinterpret_cast<__bf16*>(tl_lds + L.qst);
+  unsigned char* s_frag = tl_lds + L.frag;
+
+  const size_t qk_row = (size_t)a.Hk * D, v_row = (size_t)a.Hv * D;
+  const __bf16* Qb = reinterpret_cast<const __bf16*>(a.q) + (size_t)off * qk_row + (size_t)hq * D;
+  const __bf16* Kb = reinterpret_cast<const __bf16*>(a.k) + (size_t)off * qk_row + (size_t)hq * D;
+  const __bf16* Vb = reinterpret_cast<const __bf16*>(a.v) + (size_t)off * v_row + (size_t)h * D;
+
+  // ---- prologue, batch 1: parents and gates, the wave's state rows, and the
+  // V and Q rows into LDS.  Copy position p = base + lane holds 16-byte chunk
+  // swz(r, p % CPRK) of row r = p / CPRK.
+  TL_TRACE_POINT(a, 1);
+  int par = -1;
+  float gx = 0.f;
+  if (tid < T) {
+    par = a.parent[off + tid];
+    gx = a.g[(size_t)(off + tid) * a.Hv + h];
+  }
+  f32x4 sraw[KS][2];
+  if (vw) {
+    const float* row = a.state + ((size_t)sidx * a.Hv + h) * D * D + (size_t)(kTile * wave + lr) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      sraw[ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 4 * lg));
+      sraw[ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 16 + 4 * lg));
+    }
+  }
+  const int TP = (T + 31) & ~31;   // V rows of every chunk the tree reads
+  for (int base = wave * 64; base < TP * CPRK; base += NT) {   // uniform; TP * CPRK is a multiple of 64
+    const int p = base + lane, r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
+    copy16_to_lds_async(Vb + (size_t)min(r, T - 1) * v_row + c * 8, s_k + (size_t)base * 8);
+  }
+  for (int base = wave * 64; base < T * CPRK; base += NT) {   // uniform
+    const int p = base + lane;
+    if (p < T * CPRK) {
+      const int r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
+      copy16_to_lds_async(Qb + (size_t)r * qk_row + c * 8, s_q + (size_t)base * 8);
+    }
+  }
+  for (int x = tid; x < (tm / kTile) * W; x += NT) s_tmask[x] = 0;
+  wait_vmem_below<0>();   // batch 1 has landed (a wait the compiler sees)
+  lds_barrier();          // staged V rows, Q rows and zeroed tile masks are visible
+  TL_TRACE_POINT(a, 2);
+
+  // the wave's V^T operand fragments of every chunk: lane (lg, lr) names row
+  // 4 lg + lr / 4 of a 16-node half chunk and columns 16 w + 4 (lr % 4) .. + 3,
+  // so it receives value channel 16 w + lr of nodes 4 lg .. 4 lg + 3 of that
+  // half (K positions kpos(lg, 0..3) and kpos(lg, 4..7) for the two halves)
+  bf16x8 vreg[NCH];
+  {
+    const int nch = TP / 32;   // chunks that hold a node (uniform)
+    const int vrow_l = 4 * lg + (lr >> 2);
+    const int col = kTile * (vw ? wave : 0) + 4 * (lr & 3);
+    const int vo = vrow_l * D * 2 + swz<CPRK>(vrow_l, col >> 3) * 16 + (col & 7) * 2;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      bf16x8 f = bf16x8{};
+      if (vw && c < nch) {   // uniform
+        // rows 32 c + vrow_l and 32 c + 16 + vrow_l keep the swizzle key of
+        // row vrow_l (32 c and 16 are multiples of CPRK)
+        const bf16x4 x0 = lds_read_tr16(s_k, vo + (32 * c) * D * 2);
+        const bf16x4 x1 = lds_read_tr16(s_k, vo + (32 * c + 16) * D * 2);
+        f = bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+        // nodes >= T carry copies of row T - 1; their coefficients are zero,
+        // and zero values keep a non-finite input of node T - 1 from reaching
+        // other nodes through them
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int n = 32 * c + (e < 4 ? 4 * lg + e : 16 + 4 * lg + (e - 4));
+          if (n >= T) f[e] = (__bf16)0.f;
+        }
+      }
+      vreg[c] = f;
+    }
+  }
+  lds_barrier();   // every wave has read the staged V rows
+
+  // ---- batch 2: K rows over the staged V rows, while the topology is built
+  for (int base = wave * 64; base < T * CPRK; base += NT) {   // uniform
+    const int p = base + lane;
+    if (p < T * CPRK) {
+      const int r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
+      copy16_to_lds_async(Kb + (size_t)r * qk_row + c * 8, s_k + (size_t)base * 8);
+    }
+  }
+  TL_TRACE_POINT(a, 3);
+  {
+    int* s_jmp = reinterpret_cast<int*>(s_frag);
+    float* s_acc = reinterpret_cast<float*>(s_jmp + kThreads);
+    int* s_cnt = reinterpret_cast<int*>(s_acc + kThreads);
+    uint64_t* s_msk = reinterpret_cast<uint64_t*>(s_cnt + kThreads);
+    int dep = 0;
+    float cl = 0.f;
+    uint64_t msk[W];
+    const bool ok = build_topology<W, true>(par, T, gx, s_jmp, s_acc, s_cnt, s_msk, dep, cl, msk);
+    if (!ok) {
+      if (tid == 0) report(a.dev_err, TL_EBADTREE);
+      wait_vmem();   // let the in-flight LDS copies land before the block retires
+      return;
+    }
+    if (tid < tm) {   // rows past T: zero masks and decays
+      s_cl[tid] = tid < T ? cl * kLog2e : 0.f;
+#pragma unroll
+      for (int w = 0; w < W; ++w) s_mask[tid * W + w] = tid < T ? msk[w] : 0ull;
+      if (tid < T) {
+        const int I = tid / kTile;
+#pragma unroll
+        for (int w = 0; w < W; ++w)
+          if (msk[w]) atomicOr(reinterpret_cast<unsigned long long*>(&s_tmask[I * W + w]),
+                               (unsigned long long)msk[w]);
+      }
+    }
+  }
+  // the wave's state rows, split into bf16 hi + lo MFMA A operands
+  bf16x8 shi[KS], slo[KS];
+  if (vw) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) split8_bf16(sraw[ks][0], sraw[ks][1], shi[ks], slo[ks]);
+  }
+  wait_vmem();     // batch 2 (the K rows) has landed
+  lds_barrier();   // K rows, M+ rows, tile masks and decays are visible; the topology scratch is dead
+  TL_TRACE_POINT(a, 4);
+
+  // operand fragment of row R + lr (R a multiple of 16), K chunk ks, of a
+  // swizzled LDS matrix
+  const int key = lr & (CPRK - 1);
+  const int fo_row = lr * D * 2 + (lg & 1) * 8;
+  auto frag = [&](const __bf16* base, int R, int ks) __attribute__((always_inline)) {
+    const unsigned char* p = reinterpret_cast<const unsigned char*>(base) + R * D * 2 + fo_row;
+    const bf16x4 x0 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + (lg >> 1)) ^ key) * 16));
+    const bf16x4 x1 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + 2 + (lg >> 1)) ^ key) * 16));
+    return bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+  };
+  // 32 bits of tile I's OR mask starting at node 32 c (uniform)
+  auto tile_bits32 = [&](int I, int c) __attribute__((always_inline)) {
+    return (unsigned)(s_tmask[I * W + (c >> 1)] >> ((c & 1) * 32));
+  };
+
+  // (a) coefficient chunks of tile I into buf: half chunk J (tiles 0 ..
+  // 2 (I / 2) + 1) goes to wave J % NW, so a wave always forms the same half
+  // chunks and keeps their K_J fragments in registers once read (kreg slot
+  // J / NW).  Operand layout [chunk][hi | lo][lane] 16 bytes, half J & 1 in
+  // bytes 8 (J & 1) .. + 7.  qf holds the Q fragments of tile I.
+  constexpr int NJ = 4 * W;                     // node tiles of the largest tree
+  constexpr int NKS = (NJ + NW - 1) / NW;       // half chunks per wave
+  bf16x8 kreg[NKS][KS];
+  auto chunks = [&](int I, const bf16x8 (&qf)[KS], unsigned char* buf) __attribute__((always_inline)) {
+    const int nh = 2 * (I / 2 + 1);
+    const int i = kTile * I + lr;
+    const float cli = s_cl[i];
+#pragma unroll
+    for (int sl = 0; sl < NKS; ++sl) {
+      const int J = wave + sl * NW;
+      if (J >= nh) break;   // uniform
+      const int c = J >> 1, hf = J & 1;
+      const unsigned cbits = tile_bits32(I, c);
+      if (!cbits) continue;   // a chunk without an ancestor of the tile is never read
+      const unsigned bits = (cbits >> (hf * kTile)) & 0xFFFFu;
+      float cv[4] = {0.f, 0.f, 0.f, 0.f};
+      if (J <= I && bits) {   // uniform
+        if (J == I) {         // first use of tile J (its own diagonal block is never empty)
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) kreg[sl][ks] = frag(s_k, kTile * J, ks);
+        }
+        f32x4 qk = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qk = mfma16(kreg[sl][ks], qf[ks], qk);   // rows j, column i
+        const uint64_t mw = s_mask[i * W + (J >> 2)];   // M+ row of node i (zero past T)
+        const f32x4 clj = *reinterpret_cast<const f32x4*>(s_cl + kTile * J + 4 * lg);
+        const unsigned mb = (unsigned)(mw >> ((J & 3) * kTile + 4 * lg)) & 0xFu;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          cv[r] = ((mb >> r) & 1u) ? (__builtin_amdgcn_exp2f(cli - clj[r]) * a.q_scale) * qk[r] : 0.f;
+      }
+      uint32_t cw[4];   // hi01 hi23, lo01 lo23
+      split2_bf16(cv[0], cv[1], cw[0], cw[2]);
+      split2_bf16(cv[2], cv[3], cw[1], cw[3]);
+      unsigned char* pc = buf + ((c * 2) * 64 + lane) * 16 + hf * 8;
+      *reinterpret_cast<uint2*>(pc) = uint2{cw[0], cw[1]};
+      *reinterpret_cast<uint2*>(pc + 1024) = uint2{cw[2], cw[3]};
+    }
+  };
+  // Q fragments of tile I (B operand, columns = the tile's nodes)
+  auto load_qf = [&](int I, bf16x8 (&qf)[KS]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[ks] = frag(s_q, kTile * I, ks);
+  };
+
+  // (b) value rows of this wave for tile I, from the chunk operands in buf
+  float* obase = a.out + (size_t)off * v_row + (size_t)h * D + kTile * wave + 4 * lg;
+  auto value_work = [&](int I, const bf16x8 (&qf)[KS], const unsigned char* buf) __attribute__((always_inline)) {
+    const int cI = I / 2;
+    const int i = kTile * I + lr;
+    uint32_t live = 0;   // chunks with an ancestor of tile I (uniform)
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) live |= (c <= cI && tile_bits32(I, c) != 0u ? 1u : 0u) << c;
+    live = __builtin_amdgcn_readfirstlane(live);
+    const float cli = s_cl[i];
+    f32x4 b0h = f32x4{0.f, 0.f, 0.f, 0.f}, b0l = b0h, acc = b0h, acc2 = b0h;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      b0h = mfma16(shi[ks], qf[ks], b0h);
+      b0l = mfma16(slo[ks], qf[ks], b0l);
+    }
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {   // V^T from registers: a static chunk index
+      if (!((live >> c) & 1u)) continue;   // uniform
+      const unsigned char* pc = buf + ((c * 2) * 64 + lane) * 16;
+      const bf16x8 ch = *reinterpret_cast<const bf16x8*>(pc);
+      const bf16x8 cl = *reinterpret_cast<const bf16x8*>(pc + 1024);
+      acc = mfma16(vreg[c], ch, acc);
+      acc2 = mfma16(vreg[c], cl, acc2);
+    }
+    if (i < T) {
+      const float ps = __builtin_amdgcn_exp2f(cli) * a.q_scale;
+      f32x4 o;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) o[r] = ps * (b0h[r] + b0l[r]) + (acc[r] + acc2[r]);
+      store_out<false>(obase + (size_t)i * v_row, o);
+    }
+  };
+
+  // Every wave reads the Q fragments of the tile whose chunks it forms and
+  // keeps them for that tile's value work one phase later.
+  auto bufp = [&](int I) { return (DB && (I & 1)) ? tl_lds + L.frag2 : s_frag; };
+  const int nt = (T + kTile - 1) / kTile;
+  bf16x8 qcur[KS], qnext[KS];
+  load_qf(0, qcur);
+  chunks(0, qcur, bufp(0));
+  lds_barrier();
+  TL_TRACE_POINT(a, 5);
+  for (int I = 0; I < nt; ++I) {   // uniform
+    if constexpr (DB) {
+      if (I + 1 < nt) {
+        load_qf(I + 1, qnext);
+        chunks(I + 1, qnext, bufp(I + 1));
+      }
+      if (vw) value_work(I, qcur, bufp(I));
+      lds_barrier();   // chunks of tile I + 1 visible; buffer I & 1 free again
+    } else {
+      if (vw) value_work(I, qcur, s_frag);
+      if (I + 1 < nt) {
+        load_qf(I + 1, qnext);
+        lds_barrier();   // every wave is done with the chunk buffer
+        chunks(I + 1, qnext, s_frag);
+        lds_barrier();   // chunks of tile I + 1 are in LDS
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qcur[ks] = qnext[ks];
+    if (I == 0) TL_TRACE_POINT(a, 6);
+  }
+  TL_TRACE_POINT(a, 15);
+}
+
+// LDS bytes of the kernel for a node cap (double-buffered if that fits).
+int verify_gla_large_lds_bytes(int d, int tm) {
+  const int W = tm > 128 ? 4 : (tm > 64 ? 2 : 1);
+  const int db = gla_large_layout(d, tm, W, true).total;
+  return db <= 160 * 1024 ? db : gla_large_layout(d, tm, W, false).total;
+}
+
+template <int D, int W, bool DB>
+static tl_status launch_gla_large_one(const VerifyArgs& a, hipStream_t stream) {
+  const int lds = gla_large_layout(D, a.tm, W, DB).total;
+  if (lds > 160 * 1024) return TL_EUNSUPPORTED;
+  const long blocks = 8 * (((long)a.batch * a.Hk + 7) / 8) * (a.Hv / a.Hk);
+  if (blocks == 0) return TL_OK;
+  if (blocks > 0x7fffffffL) return TL_EINVAL;
+  auto kern = verify_gla_large_kernel<D, W, DB>;
+  if (lds > 64 * 1024) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess)
+      return TL_EHIP;
+  }
+  VerifyArgs b = a;
+  b.lds_bytes = lds;
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64 * gla_large_waves(D)), lds, stream, b);
+  return hipGetLastError() == hipSuccess ? TL_OK : TL_EHIP;
+}
+
+template <int D, int W>
+static tl_status launch_gla_large_db(const VerifyArgs& a, hipStream_t stream) {
+  if (gla_large_layout(D, a.tm, W, true).total <= 160 * 1024) return launch_gla_large_one<D, W, true>(a, stream);
+  return launch_gla_large_one<D, W, false>(a, stream);
+}
+
+template <int D>
+static tl_status launch_gla_large_w(const VerifyArgs& a, hipStream_t stream) {
+  if (a.tm > 128) return launch_gla_large_db<D, 4>(a, stream);
+  return launch_gla_large_db<D, 2>(a, stream);
+}
+
+tl_status launch_verify_gla_large(const tl_problem& p, const VerifyArgs& a, hipStream_t stream) {
+  if (a.tm <= 64 || a.tm > 256) return TL_EUNSUPPORTED;
+  switch (p.d_k) {
+    case 32: return launch_gla_large_w<32>(a, stream);
+    case 64: return launch_gla_large_w<64>(a, stream);
+    case 128: return launch_gla_large_w<128>(a, stream);
+    default: return TL_EUNSUPPORTED;
+  }
+}
+
+}  // namespace tl
