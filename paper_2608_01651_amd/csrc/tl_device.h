@@ -3,8 +3,9 @@
 
 #include <hip/hip_runtime.h>
 
-#include <type_traits>
 #include <stdint.h>
+#include <type_traits>
+#include <utility>
 
 #include "treelin.h"
 
@@ -26,6 +27,16 @@
 #endif
 
 namespace tl {
+
+// f(std::integral_constant<int, J>{}) for J = 0 .. N-1, in order.
+template <class F, int... J>
+__device__ inline void static_for_seq(F& f, std::integer_sequence<int, J...>) {
+  (f(std::integral_constant<int, J>{}), ...);
+}
+template <int N, class F>
+__device__ inline void static_for(F& f) {
+  static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
 
 constexpr int kThreads = 256;      // every kernel runs 4 wave64s per workgroup
 constexpr int kWaves = kThreads / 64;

@@ -81,15 +81,6 @@ __host__ __device__ constexpr int tri(int n) { return n * (n + 1) / 2; }
 __host__ __device__ constexpr int pair_row(int I) { return (I / 2) * (I / 2 + 1) + ((I & 1) ? I / 2 + 1 : 0); }
 __host__ __device__ constexpr int gpair_row(int I) { return (I / 2) * (I / 2) + ((I & 1) ? I / 2 : 0); }
 
-template <class F, int... J>
-__device__ inline void static_for_seq(F& f, std::integer_sequence<int, J...>) {
-  (f(std::integral_constant<int, J>{}), ...);
-}
-template <int N, class F>
-__device__ inline void static_for(F& f) {
-  static_for_seq(f, std::make_integer_sequence<int, N>{});
-}
-
 }  // namespace
 
 struct DenseLayout {

@@ -56,9 +56,17 @@ struct GlaLargeLayout {
   int cl, mask, tmask, kst, qst, frag, fragsz, frag2, total;
 };
 
-// LDS layout (bytes); identical on host and device.  With db the chunk
-// operands are double-buffered.
-__host__ __device__ inline GlaLargeLayout gla_large_layout(int D, int tm, int W, bool db) {
+// Where the chunk operands of odd node tiles go.  kBufTwo: a second buffer
+// after the first; kBufK: the start of the K region.
+// A wave reads the K rows of tile J once, into registers, when it forms the
+// half chunks of tile J (the diagonal block is never empty), so when the
+// chunks of tile I are formed the K rows of tiles 0..I - 1 are dead, and
+// the I + 1 KB the operands of an odd tile I take lie below the rows of tile
+// I at d >= 64.
+enum GlaLargeBuf { kBufTwo = 1, kBufK = 2 };
+
+// LDS layout (bytes); identical on host and device.
+__host__ __device__ inline GlaLargeLayout gla_large_layout(int D, int tm, int W, int buf) {
   GlaLargeLayout L;
   int o = 0;
   L.cl = o;    o += align16(tm * 4);                     // cumulative log2-decay (0 past T)
@@ -69,14 +77,20 @@ __host__ __device__ inline GlaLargeLayout gla_large_layout(int D, int tm, int W,
   L.frag = o;                                            // chunk operands | topology scratch
   L.fragsz = ((tm + 31) / 32) * 2 * 1024;                // chunks of tiles 0..I: C hi, C lo
   const int topo = kThreads * (4 + 4 + 4) + kThreads * W * 8;
-  const int fr = (db ? 2 : 1) * L.fragsz;
+  const int fr = (buf == kBufTwo ? 2 : 1) * L.fragsz;
   o += align16(fr > topo ? fr : topo);
-  L.frag2 = db ? L.frag + L.fragsz : L.frag;
+  L.frag2 = buf == kBufTwo ? L.frag + L.fragsz : (buf == kBufK ? L.kst : L.frag);
   L.total = o;
   return L;
 }
 
-template <int D, int W, bool DB>
+// The buffering of a problem: two buffers where LDS holds them, else the K
+// region (d >= 64; at d = 32 two buffers always fit).
+__host__ __device__ inline int gla_large_buf(int D, int tm, int W) {
+  return gla_large_layout(D, tm, W, kBufTwo).total <= 160 * 1024 ? kBufTwo : kBufK;
+}
+
+template <int D, int W, int BUF>
 __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kernel(VerifyArgs a) {
   constexpr int NW = gla_large_waves(D);
   constexpr int NT = 64 * NW;
@@ -111,7 +125,7 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kern
     return;
   }
   const int tm = a.tm;
-  const GlaLargeLayout L = gla_large_layout(D, tm, W, DB);
+  const GlaLargeLayout L = gla_large_layout(D, tm, W, BUF);
   float* s_cl = reinterpret_cast<float*>(tl_lds + L.cl);
   uint64_t* s_mask = reinterpret_cast<uint64_t*>(tl_lds + L.mask);
   uint64_t* s_tmask = reinterpret_cast<uint64_t*>(tl_lds + L.tmask);
@@ -249,21 +263,30 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kern
     const bf16x4 x1 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + 2 + (lg >> 1)) ^ key) * 16));
     return bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
   };
-  // 32 bits of tile I's OR mask starting at node 32 c (uniform)
+  // the tile masks, word x in lane x (at most 64 words), and 32 bits of tile
+  // I's mask starting at node 32 c, read across lanes (uniform)
+  const uint64_t tmv = lane < (tm / kTile) * W ? s_tmask[lane] : 0ull;
   auto tile_bits32 = [&](int I, int c) __attribute__((always_inline)) {
-    return (unsigned)(s_tmask[I * W + (c >> 1)] >> ((c & 1) * 32));
+    const int x = I * W + (c >> 1);
+    return (c & 1) ? (unsigned)__builtin_amdgcn_readlane((int)(uint32_t)(tmv >> 32), x)
+                   : (unsigned)__builtin_amdgcn_readlane((int)(uint32_t)tmv, x);
   };
 
   // (a) coefficient chunks of tile I into buf: half chunk J (tiles 0 ..
   // 2 (I / 2) + 1) goes to wave J % NW, so a wave always forms the same half
   // chunks and keeps their K_J fragments in registers once read (kreg slot
-  // J / NW).  Operand layout [chunk][hi | lo][lane] 16 bytes, half J & 1 in
-  // bytes 8 (J & 1) .. + 7.  qf holds the Q fragments of tile I.
+  // J / NW).  Half chunks without an ancestor of the tile are stored as
+  // zeros, so the value work reads every chunk 0 .. I / 2 without a test.
+  // Operand layout [chunk][hi | lo][lane] 16 bytes, half J & 1 in bytes
+  // 8 (J & 1) .. + 7.  qf holds the Q fragments of tile I.  The tile index is
+  // a compile-time constant (the tile loop is unrolled), so every chunk
+  // count is one too.
   constexpr int NJ = 4 * W;                     // node tiles of the largest tree
   constexpr int NKS = (NJ + NW - 1) / NW;       // half chunks per wave
   bf16x8 kreg[NKS][KS];
-  auto chunks = [&](int I, const bf16x8 (&qf)[KS], unsigned char* buf) __attribute__((always_inline)) {
-    const int nh = 2 * (I / 2 + 1);
+  auto chunks = [&](auto Ic, const bf16x8 (&qf)[KS], unsigned char* buf) __attribute__((always_inline)) {
+    constexpr int I = decltype(Ic)::value;
+    constexpr int nh = 2 * (I / 2 + 1);
     const int i = kTile * I + lr;
     const float cli = s_cl[i];
 #pragma unroll
@@ -271,9 +294,7 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kern
       const int J = wave + sl * NW;
       if (J >= nh) break;   // uniform
       const int c = J >> 1, hf = J & 1;
-      const unsigned cbits = tile_bits32(I, c);
-      if (!cbits) continue;   // a chunk without an ancestor of the tile is never read
-      const unsigned bits = (cbits >> (hf * kTile)) & 0xFFFFu;
+      const unsigned bits = (tile_bits32(I, c) >> (hf * kTile)) & 0xFFFFu;
       float cv[4] = {0.f, 0.f, 0.f, 0.f};
       if (J <= I && bits) {   // uniform
         if (J == I) {         // first use of tile J (its own diagonal block is never empty)
@@ -304,15 +325,21 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kern
     for (int ks = 0; ks < KS; ++ks) qf[ks] = frag(s_q, kTile * I, ks);
   };
 
-  // (b) value rows of this wave for tile I, from the chunk operands in buf
+  // (b) value rows of this wave for tile I, from the chunk operands in buf:
+  // the operands of chunks 0 .. I / 2 are all requested first, so their LDS
+  // latency overlaps one another and the state term's products
   float* obase = a.out + (size_t)off * v_row + (size_t)h * D + kTile * wave + 4 * lg;
-  auto value_work = [&](int I, const bf16x8 (&qf)[KS], const unsigned char* buf) __attribute__((always_inline)) {
-    const int cI = I / 2;
+  auto value_work = [&](auto Ic, const bf16x8 (&qf)[KS], const unsigned char* buf) __attribute__((always_inline)) {
+    constexpr int I = decltype(Ic)::value;
+    constexpr int NC = I / 2 + 1;
     const int i = kTile * I + lr;
-    uint32_t live = 0;   // chunks with an ancestor of tile I (uniform)
+    bf16x8 ch[NC], cl[NC];
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) live |= (c <= cI && tile_bits32(I, c) != 0u ? 1u : 0u) << c;
-    live = __builtin_amdgcn_readfirstlane(live);
+    for (int c = 0; c < NC; ++c) {
+      const unsigned char* pc = buf + ((c * 2) * 64 + lane) * 16;
+      ch[c] = *reinterpret_cast<const bf16x8*>(pc);
+      cl[c] = *reinterpret_cast<const bf16x8*>(pc + 1024);
+    }
     const float cli = s_cl[i];
     f32x4 b0h = f32x4{0.f, 0.f, 0.f, 0.f}, b0l = b0h, acc = b0h, acc2 = b0h;
 #pragma unroll
@@ -321,13 +348,9 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kern
       b0l = mfma16(slo[ks], qf[ks], b0l);
     }
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {   // V^T from registers: a static chunk index
-      if (!((live >> c) & 1u)) continue;   // uniform
-      const unsigned char* pc = buf + ((c * 2) * 64 + lane) * 16;
-      const bf16x8 ch = *reinterpret_cast<const bf16x8*>(pc);
-      const bf16x8 cl = *reinterpret_cast<const bf16x8*>(pc + 1024);
-      acc = mfma16(vreg[c], ch, acc);
-      acc2 = mfma16(vreg[c], cl, acc2);
+    for (int c = 0; c < NC; ++c) {   // V^T from registers
+      acc = mfma16(vreg[c], ch[c], acc);
+      acc2 = mfma16(vreg[c], cl[c], acc2);
     }
     if (i < T) {
       const float ps = __builtin_amdgcn_exp2f(cli) * a.q_scale;
@@ -338,54 +361,55 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kern
     }
   };
 
-  // Every wave reads the Q fragments of the tile whose chunks it forms and
-  // keeps them for that tile's value work one phase later.
-  auto bufp = [&](int I) { return (DB && (I & 1)) ? tl_lds + L.frag2 : s_frag; };
+  // Each step forms the chunks of tile I + 1 (buffer (I + 1) & 1, free since
+  // the previous barrier) while the value work of tile I reads buffer I & 1:
+  // one barrier per tile.  Every wave reads the Q fragments of the tile whose
+  // chunks it forms and keeps them for that tile's value work.
   const int nt = (T + kTile - 1) / kTile;
   bf16x8 qcur[KS], qnext[KS];
   load_qf(0, qcur);
-  chunks(0, qcur, bufp(0));
+  chunks(std::integral_constant<int, 0>{}, qcur, s_frag);
   lds_barrier();
   TL_TRACE_POINT(a, 5);
-  for (int I = 0; I < nt; ++I) {   // uniform
-    if constexpr (DB) {
+  auto step = [&](auto Ic) __attribute__((always_inline)) {
+    constexpr int I = decltype(Ic)::value;
+    if (I >= nt) return;   // uniform
+    unsigned char* bnext = ((I + 1) & 1) ? tl_lds + L.frag2 : s_frag;
+    const unsigned char* bcur = (I & 1) ? tl_lds + L.frag2 : s_frag;
+    if (I == 9) TL_TRACE_POINT(a, 7);
+    if constexpr (I + 1 < NJ) {
       if (I + 1 < nt) {
         load_qf(I + 1, qnext);
-        chunks(I + 1, qnext, bufp(I + 1));
-      }
-      if (vw) value_work(I, qcur, bufp(I));
-      lds_barrier();   // chunks of tile I + 1 visible; buffer I & 1 free again
-    } else {
-      if (vw) value_work(I, qcur, s_frag);
-      if (I + 1 < nt) {
-        load_qf(I + 1, qnext);
-        lds_barrier();   // every wave is done with the chunk buffer
-        chunks(I + 1, qnext, s_frag);
-        lds_barrier();   // chunks of tile I + 1 are in LDS
+        chunks(std::integral_constant<int, I + 1>{}, qnext, bnext);
       }
     }
+    if (I == 9) TL_TRACE_POINT(a, 8);
+    if (vw) value_work(Ic, qcur, bcur);
+    if (I == 9) TL_TRACE_POINT(a, 9);
+    lds_barrier();   // chunks of tile I + 1 visible; buffer I & 1 free again
+    if (I == 9) TL_TRACE_POINT(a, 10);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) qcur[ks] = qnext[ks];
     if (I == 0) TL_TRACE_POINT(a, 6);
-  }
+  };
+  static_for<NJ>(step);
   TL_TRACE_POINT(a, 15);
 }
 
-// LDS bytes of the kernel for a node cap (double-buffered if that fits).
+// LDS bytes of the kernel for a node cap.
 int verify_gla_large_lds_bytes(int d, int tm) {
   const int W = tm > 128 ? 4 : (tm > 64 ? 2 : 1);
-  const int db = gla_large_layout(d, tm, W, true).total;
-  return db <= 160 * 1024 ? db : gla_large_layout(d, tm, W, false).total;
+  return gla_large_layout(d, tm, W, gla_large_buf(d, tm, W)).total;
 }
 
-template <int D, int W, bool DB>
+template <int D, int W, int BUF>
 static tl_status launch_gla_large_one(const VerifyArgs& a, hipStream_t stream) {
-  const int lds = gla_large_layout(D, a.tm, W, DB).total;
+  const int lds = gla_large_layout(D, a.tm, W, BUF).total;
   if (lds > 160 * 1024) return TL_EUNSUPPORTED;
   const long blocks = 8 * (((long)a.batch * a.Hk + 7) / 8) * (a.Hv / a.Hk);
   if (blocks == 0) return TL_OK;
   if (blocks > 0x7fffffffL) return TL_EINVAL;
-  auto kern = verify_gla_large_kernel<D, W, DB>;
+  auto kern = verify_gla_large_kernel<D, W, BUF>;
   if (lds > 64 * 1024) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                             hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess)
@@ -398,15 +422,16 @@ static tl_status launch_gla_large_one(const VerifyArgs& a, hipStream_t stream) {
 }
 
 template <int D, int W>
-static tl_status launch_gla_large_db(const VerifyArgs& a, hipStream_t stream) {
-  if (gla_large_layout(D, a.tm, W, true).total <= 160 * 1024) return launch_gla_large_one<D, W, true>(a, stream);
-  return launch_gla_large_one<D, W, false>(a, stream);
+static tl_status launch_gla_large_buf(const VerifyArgs& a, hipStream_t stream) {
+  if (gla_large_buf(D, a.tm, W) == kBufTwo) return launch_gla_large_one<D, W, kBufTwo>(a, stream);
+  if constexpr (D >= 64) return launch_gla_large_one<D, W, kBufK>(a, stream);
+  return TL_EUNSUPPORTED;
 }
 
 template <int D>
 static tl_status launch_gla_large_w(const VerifyArgs& a, hipStream_t stream) {
-  if (a.tm > 128) return launch_gla_large_db<D, 4>(a, stream);
-  return launch_gla_large_db<D, 2>(a, stream);
+  if (a.tm > 128) return launch_gla_large_buf<D, 4>(a, stream);
+  return launch_gla_large_buf<D, 2>(a, stream);
 }
 
 tl_status launch_verify_gla_large(const tl_problem& p, const VerifyArgs& a, hipStream_t stream) {

@@ -35,23 +35,11 @@
 // once, split into bf16 hi + lo in registers.
 #include <hip/hip_runtime.h>
 
-#include <utility>
-
 #include "tl_device.h"
 #include "tl_kernels.h"
 #include "verify_common.h"
 
 namespace tl {
-
-// f(std::integral_constant<int, J>{}) for J = 0 .. N-1, in order.
-template <class F, int... J>
-__device__ inline void static_for_seq(F& f, std::integer_sequence<int, J...>) {
-  (f(std::integral_constant<int, J>{}), ...);
-}
-template <int N, class F>
-__device__ inline void static_for(F& f) {
-  static_for_seq(f, std::make_integer_sequence<int, N>{});
-}
 
 __host__ __device__ constexpr int tiled_waves(int D) { return D / kTile > kWaves ? D / kTile : kWaves; }
 
