@@ -168,7 +168,7 @@ __device__ inline bool load_request(const int32_t* node_offsets, int b, int max_
 }
 
 // ---------------------------------------------------------------------------
-// Topology by pointer jumping over the parent array (one thread per node).
+// Topology over the parent array (one thread per node).
 //
 // `par` is node i's parent (any value for threads i >= T).
 // Computes, for node i = threadIdx.x < T:
@@ -176,29 +176,56 @@ __device__ inline bool load_request(const int32_t* node_offsets, int b, int max_
 //   cl     = sum of x over Anc(i) u {i}   (the cumulative log-decay when x = g,
 //            so P_i = exp(cl_i) and P_i / P_j = exp(cl_i - cl_j)),
 //   mask   = the M+ row of i as W little-endian 64-bit words.
-// After round r every node has folded in the 2^r nodes above it, so the loop
-// ends after ceil(log2(depth + 1)) rounds; all threads take part in every
-// barrier.  Returns false (uniformly) if any parent breaks the
-// parent-before-child order.  Scratch arrays need kThreads entries
-// (kThreads * W words for the mask scratch).
+// Every node first walks up its own root path through the parents in LDS,
+// folding in one ancestor per step with no barrier (a wave runs as many steps
+// as its deepest node needs), for at most kTopoWalk steps.  A node's state
+// then covers the path segment from itself up to (excluding) jmp.  Nodes
+// still short of the root finish by pointer jumping over those segments:
+// after round r a node has folded in 2^r segments above it, and all threads
+// take part in every barrier.  Returns false (uniformly) if any parent
+// breaks the parent-before-child order.  Scratch arrays need kThreads
+// entries (kThreads * W words for the mask scratch).
 // ---------------------------------------------------------------------------
+constexpr int kTopoWalk = 16;
+
 template <int W, bool WANT_MASK>
 __device__ inline bool build_topology(int par, int T, float x,
                                       int32_t* s_jmp, float* s_acc, int32_t* s_cnt,
                                       uint64_t* s_msk, int& depth, float& cl,
                                       uint64_t (&mask)[W]) {
   const int i = threadIdx.x;
-  const bool bad = (i < T) && !(par == -1 || (par >= 0 && par < i));
-  if (__syncthreads_or(bad)) return false;
+  const bool live = i < T;
+  const bool bad = live && !(par == -1 || (par >= 0 && par < i));
+  if (live) {   // parents and own values, read by the walks of descendants
+    s_jmp[i] = par;
+    s_acc[i] = x;
+  }
+  if (__syncthreads_or(bad)) return false;   // also orders the stores above before the walks
 
-  int jmp = par;
+  int jmp = live ? par : -1;
   int cnt = 1;
   cl = x;
 #pragma unroll
-  for (int w = 0; w < W; ++w) mask[w] = (i < T && WANT_MASK && (i >> 6) == w) ? (1ull << (i & 63)) : 0ull;
+  for (int w = 0; w < W; ++w) mask[w] = (live && WANT_MASK && (i >> 6) == w) ? (1ull << (i & 63)) : 0ull;
 
-  while (__syncthreads_or(i < T && jmp >= 0)) {
-    if (i < T) {
+  for (int s = 0; s < kTopoWalk; ++s) {
+    if (__ballot(jmp >= 0) == 0ull) break;   // uniform: every node of the wave is at its root
+    if (jmp >= 0) {
+      const int up = s_jmp[jmp];
+      cl += s_acc[jmp];
+      cnt += 1;
+      if constexpr (WANT_MASK) {
+#pragma unroll
+        for (int w = 0; w < W; ++w) mask[w] |= ((jmp >> 6) == w) ? (1ull << (jmp & 63)) : 0ull;
+      }
+      jmp = up;
+    }
+  }
+
+  // the loop test is a barrier: no segment is stored before every walk (and
+  // every partner read of the previous round) is done
+  while (__syncthreads_or(live && jmp >= 0)) {
+    if (live) {
       s_jmp[i] = jmp;
       s_acc[i] = cl;
       s_cnt[i] = cnt;
@@ -208,7 +235,7 @@ __device__ inline bool build_topology(int par, int T, float x,
       }
     }
     __syncthreads();
-    if (i < T && jmp >= 0) {
+    if (live && jmp >= 0) {
       cl += s_acc[jmp];
       cnt += s_cnt[jmp];
       if constexpr (WANT_MASK) {

@@ -9,8 +9,9 @@
 //   kTopoWaveN  wave_topology_n, one wavefront, ballot + shuffle pointer
 //               jumping: gated linear attention over node caps of <= 64
 //               (bf16, d >= 32), the small-tree MFMA kernel;
-//   kTopoLds    build_topology<W>, LDS pointer jumping over one thread per
-//               node: the large-tree kernel of gated linear attention (caps
+//   kTopoLds    build_topology<W>, one thread per node: root-path walks
+//               through the parents in LDS, finished by pointer jumping for
+//               deep trees: the large-tree kernel of gated linear attention (caps
 //               of 65..256), the delta rule's tile walk (where its layout
 //               fits LDS), and the vector path (fp32 inputs or d = 16), whose
 //               own pass counts depths without masks;

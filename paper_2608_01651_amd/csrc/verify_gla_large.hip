@@ -138,8 +138,8 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kern
   const __bf16* Kb = reinterpret_cast<const __bf16*>(a.k) + (size_t)off * qk_row + (size_t)hq * D;
   const __bf16* Vb = reinterpret_cast<const __bf16*>(a.v) + (size_t)off * v_row + (size_t)h * D;
 
-  // ---- prologue, batch 1: parents and gates, the wave's state rows, and the
-  // V and Q rows into LDS.  Copy position p = base + lane holds 16-byte chunk
+  // ---- prologue, batch 1: parents and gates, the V and Q rows into LDS,
+  // and the wave's state rows.  Copy position p = base + lane holds 16-byte chunk
   // swz(r, p % CPRK) of row r = p / CPRK.
   TL_TRACE_POINT(a, 1);
   int par = -1;
@@ -147,15 +147,6 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kern
   if (tid < T) {
     par = a.parent[off + tid];
     gx = a.g[(size_t)(off + tid) * a.Hv + h];
-  }
-  f32x4 sraw[KS][2];
-  if (vw) {
-    const float* row = a.state + ((size_t)sidx * a.Hv + h) * D * D + (size_t)(kTile * wave + lr) * D;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      sraw[ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 4 * lg));
-      sraw[ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 16 + 4 * lg));
-    }
   }
   const int TP = (T + 31) & ~31;   // V rows of every chunk the tree reads
   for (int base = wave * 64; base < TP * CPRK; base += NT) {   // uniform; TP * CPRK is a multiple of 64
@@ -169,8 +160,22 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kern
       copy16_to_lds_async(Qb + (size_t)r * qk_row + c * 8, s_q + (size_t)base * 8);
     }
   }
+  // the wave's state rows last: the batch's wait leaves them in flight, and
+  // they are first read after the topology
+  f32x4 sraw[KS][2];
+  if (vw) {
+    const float* row = a.state + ((size_t)sidx * a.Hv + h) * D * D + (size_t)(kTile * wave + lr) * D;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      sraw[ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 4 * lg));
+      sraw[ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 16 + 4 * lg));
+    }
+  }
   for (int x = tid; x < (tm / kTile) * W; x += NT) s_tmask[x] = 0;
-  wait_vmem_below<0>();   // batch 1 has landed (a wait the compiler sees)
+  // batch 1 but the state rows has landed (loads complete in issue order; a
+  // wait the compiler sees, so it knows the parents and gates are in)
+  if (vw) wait_vmem_below<2 * KS>();
+  else wait_vmem_below<0>();
   lds_barrier();          // staged V rows, Q rows and zeroed tile masks are visible
   TL_TRACE_POINT(a, 2);
 
@@ -205,6 +210,7 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kern
       vreg[c] = f;
     }
   }
+  TL_TRACE_POINT(a, 11);
   lds_barrier();   // every wave has read the staged V rows
 
   // ---- batch 2: K rows over the staged V rows, while the topology is built
@@ -230,6 +236,7 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kern
       wait_vmem();   // let the in-flight LDS copies land before the block retires
       return;
     }
+    TL_TRACE_POINT(a, 13);
     if (tid < tm) {   // rows past T: zero masks and decays
       s_cl[tid] = tid < T ? cl * kLog2e : 0.f;
 #pragma unroll
@@ -249,6 +256,7 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kern
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) split8_bf16(sraw[ks][0], sraw[ks][1], shi[ks], slo[ks]);
   }
+  TL_TRACE_POINT(a, 14);
   wait_vmem();     // batch 2 (the K rows) has landed
   lds_barrier();   // K rows, M+ rows, tile masks and decays are visible; the topology scratch is dead
   TL_TRACE_POINT(a, 4);
