@@ -18,15 +18,16 @@
 // (request, v-head) runs three phases separated by two barriers:
 //  1. every wave forms its share of the 16 x 16 blocks (I, J <= I) of C and G
 //     (K_J Q_I^T and K_J K_I^T on MFMA, masked by the M+ rows, decayed) into
-//     LDS in MFMA operand order, then computes, for its own 16 value
+//     LDS in MFMA operand order, and of the in-tile inverses (I + G_II)^{-1}
+//     (forward substitution on the identity, each step broadcasting a column
+//     of the tile along its 16-lane row by DPP); then, for its own 16 value
 //     channels, B0 = Q S^T and SK = K S^T over all node tiles (state in bf16
 //     hi + lo) and R from SK;
-//  2. wave J solves column block J of A: for I = J, J + 1, ...,
+//  2. wave J forms column block J of A: for I = J, J + 1, ...,
 //       X_I = (I + G_II)^{-1} (delta_IJ - sum_{J <= K < I} G_IK X_K),
-//     the sum on MFMA, the in-tile part by forward substitution over the
-//     tile's in-tile ancestors (each step broadcasts a column of the tile
-//     along its 16-lane row by DPP).  Columns are independent, so the waves
-//     need no barrier between them.  A goes to LDS over the dead Q and K rows;
+//     all on MFMA: X_K come out of the products as the B operands of the
+//     next ones.  Columns are independent, so the waves need no barrier
+//     between them.  A goes to LDS over the dead Q and K rows;
 //  3. every wave forms U = A R and O = q_scale (P B0 + C U) for its value
 //     channels: products of LDS operands (A, C) with register operands (R,
 //     U), no LDS round trip for the value side.
@@ -45,7 +46,7 @@ namespace tl {
 
 namespace {
 
-constexpr int kDenseWaves = 8;
+constexpr int kDenseWaves = 8;                     // one per 16 value channels (d = 128)
 constexpr int kDenseThreads = 64 * kDenseWaves;
 constexpr int kDenseMaxTiles = 8;   // 128 nodes
 
@@ -84,7 +85,7 @@ __host__ __device__ constexpr int gpair_row(int I) { return (I / 2) * (I / 2) + 
 }  // namespace
 
 struct DenseLayout {
-  int cl, beta, mask, tmask, tin, gin, kq, cst, gst, xs, total;
+  int cl, beta, mask, tmask, tin, gin, kq, cst, gst, ainv, total;
 };
 
 // LDS layout (bytes); identical on host and device.
@@ -103,19 +104,25 @@ __host__ __device__ inline DenseLayout dense_layout(int tm, int W) {
     const int rows = 2 * tm * 128 * 2, ablk = pair_row(nb) * 2048;
     o += rows > ablk ? rows : ablk;
   }
-  L.cst = o;                                         // blocks of C | topology scratch
+  L.cst = o;                                         // blocks of C | staged V rows
   {
-    const int cb = pair_row(nb) * 2048, topo = kThreads * (4 + 4 + 4) + kThreads * W * 8;
-    o += cb > topo ? cb : topo;
+    const int cb = pair_row(nb) * 2048, vb = tm * 128 * 2;
+    o += cb > vb ? cb : vb;
   }
-  L.gst = o;   o += gpair_row(nb) * 2048;             // strictly lower blocks of -G
-  L.xs = o;    o += kDenseWaves * 1024;              // per-wave transposition buffer
+  L.gst = o;                                         // strictly lower blocks of -G | topology scratch
+  {
+    const int gb = gpair_row(nb) * 2048, topo = kThreads * (4 + 4 + 4) + kThreads * W * 8;
+    o += gb > topo ? gb : topo;
+  }
+  L.ainv = o;  o += nb * 1024;                      // (I + G_II)^-1 per node tile, bf16 hi | lo
   L.total = o;
   return L;
 }
 
 template <int W>
-__global__ __launch_bounds__(kDenseThreads) void verify_gdn_dense_kernel(VerifyArgs a) {
+// One workgroup per CU (LDS), so two waves per SIMD: the compiler may spend
+// the registers that allows on overlapping LDS reads with products.
+__global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void verify_gdn_dense_kernel(VerifyArgs a) {
   constexpr int D = 128;
   constexpr int KS = D / 32;
   constexpr int CPRK = D / 8;
@@ -159,8 +166,9 @@ __global__ __launch_bounds__(kDenseThreads) void verify_gdn_dense_kernel(VerifyA
   __bf16* s_q = s_k + tm * D;
   unsigned char* s_a = tl_lds + L.kq;      // blocks of A, over the dead K and Q rows
   unsigned char* s_c = tl_lds + L.cst;
+  __bf16* s_v = reinterpret_cast<__bf16*>(s_c);   // staged V rows, until the blocks of C are formed
   unsigned char* s_g = tl_lds + L.gst;
-  unsigned char* s_xs = tl_lds + L.xs + wave * 1024;
+  unsigned char* s_ainv = tl_lds + L.ainv;   // in-tile inverses, A operands of 16x16x16 products
 
   const size_t qk_row = (size_t)a.Hk * D, v_row = (size_t)a.Hv * D;
   const __bf16* Qb = reinterpret_cast<const __bf16*>(a.q) + (size_t)off * qk_row + (size_t)hq * D;
@@ -168,9 +176,15 @@ __global__ __launch_bounds__(kDenseThreads) void verify_gdn_dense_kernel(VerifyA
   const __bf16* Vb = reinterpret_cast<const __bf16*>(a.v) + (size_t)off * v_row + (size_t)h * D;
 
   // ---- prologue.  Loads in the order they are needed: parents and gates,
-  // K and Q rows (direct copies into swizzled LDS), the V values of the
-  // wave's channels, then the wave's state rows (needed last, in phase 1b).
+  // K, Q and V rows (direct copies into swizzled LDS), then the wave's state
+  // rows (needed last, in phase 1b).
+  // The copies are issued by the waves past the tree's nodes (waves 2..7:
+  // threads >= 128 >= T), so the waves that hold nodes wait for their
+  // parents and gates alone before the topology: the compiler does not see
+  // the copies, and loads complete in issue order.
   TL_TRACE_POINT(a, 1);
+  constexpr int kCopyWave0 = kDenseMaxTiles * kTile / 64;   // first wave without nodes
+  static_assert(kCopyWave0 < kDenseWaves, "some waves hold no node");
   int par = -1;
   float gx = 0.f, bx = 0.f;
   if (tid < T) {
@@ -178,22 +192,21 @@ __global__ __launch_bounds__(kDenseThreads) void verify_gdn_dense_kernel(VerifyA
     gx = a.g[(size_t)(off + tid) * a.Hv + h];
     bx = a.beta[(size_t)(off + tid) * a.Hv + h];
   }
-  for (int base = wave * 64; base < T * CPRK; base += kDenseThreads) {
-    const int p = base + lane;
-    if (p < T * CPRK) {
-      const int r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
-      copy16_to_lds_async(Kb + (size_t)r * qk_row + c * 8, s_k + (size_t)base * 8);
-      copy16_to_lds_async(Qb + (size_t)r * qk_row + c * 8, s_q + (size_t)base * 8);
+  if (wave >= kCopyWave0) {   // uniform
+    constexpr int CT = kDenseThreads - 64 * kCopyWave0;
+    for (int base = (wave - kCopyWave0) * 64; base < T * CPRK; base += CT) {
+      const int p = base + lane;
+      if (p < T * CPRK) {
+        const int r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
+        copy16_to_lds_async(Kb + (size_t)r * qk_row + c * 8, s_k + (size_t)base * 8);
+        copy16_to_lds_async(Qb + (size_t)r * qk_row + c * 8, s_q + (size_t)base * 8);
+      }
     }
-  }
-  // V[node 16 J + 4 lg + e][channel 16 wave + lr], rows clamped to the tree
-  bf16x4 vv[NTM];
-#pragma unroll
-  for (int J = 0; J < NTM; ++J) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int r = min(kTile * J + 4 * lg + e, T - 1);
-      vv[J][e] = Vb[(size_t)r * v_row + kTile * wave + lr];
+    // the V rows of every node tile, into the C region (rows past T repeat
+    // row T - 1; their R entries are set to zero)
+    for (int base = (wave - kCopyWave0) * 64; base < kTile * nt * CPRK; base += CT) {   // multiple of 64
+      const int p = base + lane, r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
+      copy16_to_lds_async(Vb + (size_t)min(r, T - 1) * v_row + c * 8, s_v + (size_t)base * 8);
     }
   }
   TL_TRACE_POINT(a, 6);
@@ -214,7 +227,7 @@ __global__ __launch_bounds__(kDenseThreads) void verify_gdn_dense_kernel(VerifyA
   for (int x = tid; x < (tm / kTile) * W; x += kDenseThreads) s_tmask[x] = 0;
   for (int x = tid; x < tm / kTile; x += kDenseThreads) s_tin[x] = 0u;
   {
-    int* s_jmp = reinterpret_cast<int*>(s_c);
+    int* s_jmp = reinterpret_cast<int*>(s_g);
     float* s_acc = reinterpret_cast<float*>(s_jmp + kThreads);
     int* s_cnt = reinterpret_cast<int*>(s_acc + kThreads);
     uint64_t* s_msk = reinterpret_cast<uint64_t*>(s_cnt + kThreads);
@@ -247,10 +260,23 @@ __global__ __launch_bounds__(kDenseThreads) void verify_gdn_dense_kernel(VerifyA
     }
   }
   TL_TRACE_POINT(a, 7);
-  // the K and Q copies (issued first) have landed once at most the V and
-  // state loads of this wave are outstanding
-  wait_vmem_below<4 * NTM + 2 * KS>();
-  lds_barrier();   // K, Q, masks and decays are in LDS (V and the state stay in flight)
+  // the K, Q and V copies (issued before the state loads) have landed once
+  // at most the state loads of this wave are outstanding
+  wait_vmem_below<2 * KS>();
+  lds_barrier();   // K, Q, V, masks and decays are in LDS (the state stays in flight)
+  // V[node 16 J + 4 lg + e][channel 16 wave + lr] by LDS transpose reads: lane
+  // (lg, lr) names row 16 J + 4 lg + lr / 4 and channels 16 wave + 4 (lr % 4)
+  // .. + 3, so it receives channel 16 wave + lr of nodes 16 J + 4 lg .. + 3
+  bf16x4 vv[NTM];
+  {
+    const int vrow_l = 4 * lg + (lr >> 2);
+    const int col = kTile * wave + 4 * (lr & 3);
+    const int vo = vrow_l * D * 2 + swz<CPRK>(vrow_l, col >> 3) * 16 + (col & 7) * 2;
+#pragma unroll
+    for (int J = 0; J < NTM; ++J)   // rows 16 J + vrow_l keep the swizzle key of row vrow_l
+      vv[J] = J < nt ? lds_read_tr16(s_v, vo + (kTile * J) * D * 2) : bf16x4{};
+  }
+  lds_barrier();   // every wave has read the staged V rows (the C blocks go over them)
   TL_TRACE_POINT(a, 3);
 
   // operand fragment of row R + lr of the swizzled K or Q rows (R a multiple of 16)
@@ -315,33 +341,62 @@ __global__ __launch_bounds__(kDenseThreads) void verify_gdn_dense_kernel(VerifyA
   auto row_of = [](int k) __attribute__((always_inline)) {
     return (k >= 1) + (k >= 3) + (k >= 6) + (k >= 10) + (k >= 15) + (k >= 21) + (k >= 28);
   };
-  auto form = [&](int k, f32x4& cv, f32x4& gv) __attribute__((always_inline)) {
-    const int I = row_of(k), J = k - tri(I);
-    const int i = kTile * I + lr;
-    const bool iv = i < T;
-    f32x4 qk = f32x4{0.f, 0.f, 0.f, 0.f}, kk = qk;
+  // Two blocks side by side: every LDS read of both first (their operand
+  // fragments, mask words and decays), then the four MFMA chains
+  // interleaved, then masking.
+  auto form2 = [&](int k0, int k1, f32x4 (&cv)[2], f32x4 (&gv)[2]) __attribute__((always_inline)) {
+    int I[2], J[2];
+    I[0] = row_of(k0);
+    J[0] = k0 - tri(I[0]);
+    I[1] = row_of(k1);
+    J[1] = k1 - tri(I[1]);
+    bf16x8 kj[2][KS], qi[2][KS], ki[2][KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 kj = frag(s_k, kTile * J, ks);
-      qk = mfma16(kj, frag(s_q, kTile * I, ks), qk);
-      kk = mfma16(kj, frag(s_k, kTile * I, ks), kk);
-    }
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        kj[b][ks] = frag(s_k, kTile * J[b], ks);
+        qi[b][ks] = frag(s_q, kTile * I[b], ks);
+        ki[b][ks] = frag(s_k, kTile * I[b], ks);
+      }
     // loads clamped into the arrays and the values selected, so that no
     // LDS read sits under a branch
-    const uint64_t mw0 = s_mask[min(i, tm - 1) * W + (J >> 2)];
-    const float cl0 = s_cl[i], b00 = s_beta[min(i, tm - 1)];
-    const uint64_t mw = iv ? mw0 : 0ull;
-    const unsigned mb = (unsigned)(mw >> ((J & 3) * kTile + 4 * lg)) & 0xFu;
-    const float cli = iv ? cl0 : 0.f, bi = iv ? b00 : 0.f;
-    const f32x4 clj = *reinterpret_cast<const f32x4*>(s_cl + kTile * J + 4 * lg);
+    uint64_t mw0[2];
+    float cl0[2], b00[2];
+    f32x4 clj[2];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const bool m = (mb >> r) & 1u;
-      const bool self = J == I && 4 * lg + r == lr;
-      const float dec = __builtin_amdgcn_exp2f(cli - clj[r]);
-      const float c = (dec * a.q_scale) * qk[r], g = (bi * dec) * kk[r];
-      cv[r] = m ? c : 0.f;
-      gv[r] = (m && !self) ? g : 0.f;
+    for (int b = 0; b < 2; ++b) {
+      const int i = kTile * I[b] + lr;
+      mw0[b] = s_mask[min(i, tm - 1) * W + (J[b] >> 2)];
+      cl0[b] = s_cl[i];
+      b00[b] = s_beta[min(i, tm - 1)];
+      clj[b] = *reinterpret_cast<const f32x4*>(s_cl + kTile * J[b] + 4 * lg);
+    }
+    f32x4 qk[2], kk[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) qk[b] = kk[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        qk[b] = mfma16(kj[b][ks], qi[b][ks], qk[b]);
+        kk[b] = mfma16(kj[b][ks], ki[b][ks], kk[b]);
+      }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const bool iv = kTile * I[b] + lr < T;
+      const uint64_t mw = iv ? mw0[b] : 0ull;
+      const unsigned mb = (unsigned)(mw >> ((J[b] & 3) * kTile + 4 * lg)) & 0xFu;
+      const float cli = iv ? cl0[b] : 0.f, bi = iv ? b00[b] : 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool m = (mb >> r) & 1u;
+        const bool self = J[b] == I[b] && 4 * lg + r == lr;
+        const float dec = __builtin_amdgcn_exp2f(cli - clj[b][r]);
+        const float c = (dec * a.q_scale) * qk[b][r], g = (bi * dec) * kk[b][r];
+        cv[b][r] = m ? c : 0.f;
+        gv[b][r] = (m && !self) ? g : 0.f;
+      }
     }
   };
   auto store = [&](int k, const f32x4& cv, const f32x4& gv) __attribute__((always_inline)) {
@@ -356,23 +411,55 @@ __global__ __launch_bounds__(kDenseThreads) void verify_gdn_dense_kernel(VerifyA
       else zero_half(s_g, gpair_row(I) + I / 2, 1);
     }
   };
-  // two blocks per step: independent MFMA chains in flight together (the
-  // block coordinates come without a loop, so both sit in one basic block)
+  // two blocks per step (block k goes to wave k % 8)
   for (int k = wave; k < nblk; k += 2 * kDenseWaves) {   // uniform
     const int k2 = k + kDenseWaves;
-    f32x4 c0, g0, c1, g1;
-    form(k, c0, g0);
-    form(min(k2, nblk - 1), c1, g1);
-    store(k, c0, g0);
-    if (k2 < nblk) store(k2, c1, g1);
+    f32x4 cv[2], gv[2];
+    form2(k, min(k2, nblk - 1), cv, gv);
+    store(k, cv[0], gv[0]);
+    if (k2 < nblk) store(k2, cv[1], gv[1]);
   }
+  // ---- 1a'. the in-tile inverses (I + G_II)^{-1}, by the wave that formed
+  // block (I, I) (block k = I (I + 3) / 2 goes to wave k % 8), from the
+  // in-tile block it stored itself: forward substitution on the identity
+  // over the tile's in-tile strict ancestors, in index order (lane s of each
+  // 16-lane row holds x_s and broadcasts it by DPP row_newbcast).  Lane
+  // (lr, lg) then holds row lr, columns 4 lg .. + 3 of the inverse: the A
+  // operand of a 16x16x16 product.
+  auto make_ainv = [&](auto Ic) __attribute__((always_inline)) {
+    constexpr int I = decltype(Ic)::value;
+    constexpr int kdiag = I * (I + 3) / 2;
+    if (I >= nt || kdiag % kDenseWaves != wave) return;   // uniform
+    const float* gi = s_gin + I * kTile * kTile + lr * kTile;
+    const f32x4 g0 = *reinterpret_cast<const f32x4*>(gi), g1 = *reinterpret_cast<const f32x4*>(gi + 4),
+                g2 = *reinterpret_cast<const f32x4*>(gi + 8), g3 = *reinterpret_cast<const f32x4*>(gi + 12);
+    const unsigned tin = __builtin_amdgcn_readfirstlane(s_tin[I]);
+    f32x4 y;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) y[r] = (4 * lg + r == lr) ? 1.f : 0.f;
+    auto sub = [&](auto sc) __attribute__((always_inline)) {
+      constexpr int s = decltype(sc)::value;
+      if ((tin >> s) & 1u) {   // uniform
+        const float gis = s < 4 ? g0[s & 3] : s < 8 ? g1[s & 3] : s < 12 ? g2[s & 3] : g3[s & 3];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float xs = __int_as_float(
+              __builtin_amdgcn_mov_dpp(__float_as_int(y[r]), 0x150 + s, 0xF, 0xF, false));
+          y[r] -= gis * xs;
+        }
+      }
+    };
+    static_for<kTile>(sub);
+    bf16x4 hi, lo;
+    split4_bf16(y, hi, lo);
+    *reinterpret_cast<bf16x4*>(s_ainv + I * 1024 + lane * 8) = hi;
+    *reinterpret_cast<bf16x4*>(s_ainv + I * 1024 + 512 + lane * 8) = lo;
+  };
+  static_for<NTM>(make_ainv);
   TL_TRACE_POINT(a, 8);
 
   // ---- 1b. B0 = Q S^T and SK = K S^T for this wave's channels, all node tiles
   // (rows = nodes 16 I + 4 lg + r, column = channel 16 wave + lr)
-  bf16x8 shi[KS], slo[KS];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) split8_bf16(sraw[ks][0], sraw[ks][1], shi[ks], slo[ks]);
   f32x4 b0[NTM];
   bf16x8 rph[NTM / 2], rpl[NTM / 2];   // R as B operands, tiles paired (K = nodes of 2 P, 2 P + 1)
 #pragma unroll
@@ -380,6 +467,10 @@ __global__ __launch_bounds__(kDenseThreads) void verify_gdn_dense_kernel(VerifyA
     rph[P] = bf16x8{};
     rpl[P] = bf16x8{};
   }
+  bf16x8 shi[KS], slo[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) split8_bf16(sraw[ks][0], sraw[ks][1], shi[ks], slo[ks]);
+  TL_TRACE_POINT(a, 9);
 #pragma unroll
   for (int I = 0; I < NTM; ++I) {
     b0[I] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -406,90 +497,74 @@ __global__ __launch_bounds__(kDenseThreads) void verify_gdn_dense_kernel(VerifyA
       set_half(rph[I / 2], rpl[I / 2], I & 1, rv);
     }
   }
-  lds_barrier();   // C, G and the in-tile blocks are in LDS; K and Q are dead
+  TL_TRACE_POINT(a, 10);
+  lds_barrier();   // C, G and the in-tile inverses are in LDS; K and Q are dead
   TL_TRACE_POINT(a, 4);
 
-  // ---- 2. column block J = wave of A = (I + G)^{-1}.  X^T_I (rows: columns
-  // 16 J + 4 lg + r of A; column: node i = 16 I + lr) is in MFMA output
-  // layout, which is per lane the A-operand element of A_IJ in U = A R.
-  // Every block (I, J <= I) of A is written, zero where no ancestor relation.
+  // ---- 2. column block J = wave of A = (I + G)^{-1}: for I = J, J + 1, ...
+  //   Y_I = delta_IJ - sum_{J <= K < I} G_IK X_K,   X_I = (I + G_II)^{-1} Y_I.
+  // Y and X come out of the products with row i (node of tile I) and column j
+  // (node of tile J): per lane exactly the B-operand elements of a product
+  // whose K index is i, so X_K feeds the later sums and Y feeds the in-tile
+  // inverse without any transposition.  The sums run over pairs of node
+  // tiles (16x16x32, the stored -G as A operands); A_IJ goes to LDS in
+  // A-operand layout for phase 3.  Every block (I, J <= I) of A is written,
+  // zero where no ancestor relation.
   if (wave < nt) {   // uniform
     const int J = wave;
-    bf16x8 xph[NTM / 2], xpl[NTM / 2];   // X^T_K as A operands, tiles paired (zero below J)
+    bf16x8 xph[NTM / 2], xpl[NTM / 2];   // X_K as B operands, tiles paired (zero below J)
 #pragma unroll
     for (int P = 0; P < NTM / 2; ++P) {
       xph[P] = bf16x8{};
       xpl[P] = bf16x8{};
     }
+    // X_I (row 4 lg + r, column lr) -> A_IJ in A-operand layout: lane
+    // (4 lg + r) + 16 (lr / 4), element lr % 4 of half `half`
+    auto store_a = [&](int pa, int half, const f32x4& x) __attribute__((always_inline)) {
+      bf16x4 hi, lo;
+      split4_bf16(x, hi, lo);
+      unsigned char* q = s_a + pa * 2048 + half * 8 + (lr & 3) * 2;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = 4 * lg + r + 16 * (lr >> 2);
+        *reinterpret_cast<__bf16*>(q + t * 16) = hi[r];
+        *reinterpret_cast<__bf16*>(q + 1024 + t * 16) = lo[r];
+      }
+    };
     auto step_tile = [&](auto Ic) __attribute__((always_inline)) {
       constexpr int I = decltype(Ic)::value;
       if (I < J || I >= nt) return;   // uniform
       const int pa = pair_row(I) + J / 2;
       if (I == J && (I & 1) == 0) zero_half(s_a, pa, 1);   // (I, I + 1): never a block
-      if (!live(I, J)) {              // A_IJ = 0
+      if (!live(I, J)) {              // A_IJ = 0 (and X_I stays zero)
         zero_half(s_a, pa, J & 1);
         return;
       }
-      // this lane's row of the in-tile block of G (node i = 16 I + lr)
-      const float* gi = s_gin + I * kTile * kTile + lr * kTile;
-      const f32x4 g0 = *reinterpret_cast<const f32x4*>(gi), g1 = *reinterpret_cast<const f32x4*>(gi + 4),
-                  g2 = *reinterpret_cast<const f32x4*>(gi + 8), g3 = *reinterpret_cast<const f32x4*>(gi + 12);
-      const unsigned tin = __builtin_amdgcn_readfirstlane(s_tin[I]);
+      const bf16x4 ah = *reinterpret_cast<const bf16x4*>(s_ainv + I * 1024 + lane * 8);
+      const bf16x4 al = *reinterpret_cast<const bf16x4*>(s_ainv + I * 1024 + 512 + lane * 8);
       f32x4 y, y2 = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int r = 0; r < 4; ++r) y[r] = (I == J && 4 * lg + r == lr) ? 1.f : 0.f;
-      // - sum_{K < I} X^T_K G_IK^T over tile pairs (X^T_K is zero below J and
-      // where A_KJ is; the half K = I of the last pair is zero), G stored negated
+      // - sum_{K < I} G_IK X_K over tile pairs (X_K is zero below J and where
+      // A_KJ is; the half K = I of the last pair is zero), G stored negated
 #pragma unroll
       for (int P = 0; 2 * P < I; ++P) {
-        if (2 * P + 1 < J) continue;   // uniform: both halves of X^T are zero
+        if (2 * P + 1 < J) continue;   // uniform: both halves of X are zero
         bf16x8 gh, gl;
         get_pair(s_g, gpair_row(I) + P, gh, gl);
-        y = mfma16(xph[P], gh, y);
-        y2 = mfma16(xph[P], gl, y2);
-        y = mfma16(xpl[P], gh, y);
+        y = mfma16(gh, xph[P], y);
+        y2 = mfma16(gl, xph[P], y2);
+        y = mfma16(gh, xpl[P], y);
       }
       y += y2;
-      // in-tile forward substitution: x_i -= G_is x_s over the in-tile
-      // strict ancestors s of i, in index order (lane s of each 16-lane row
-      // holds x_s and broadcasts it by DPP row_newbcast)
-      auto sub = [&](auto sc) __attribute__((always_inline)) {
-        constexpr int s = decltype(sc)::value;
-        if ((tin >> s) & 1u) {   // uniform
-          const float gis = s < 4 ? g0[s & 3] : s < 8 ? g1[s & 3] : s < 12 ? g2[s & 3] : g3[s & 3];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float xs = __int_as_float(
-                __builtin_amdgcn_mov_dpp(__float_as_int(y[r]), 0x150 + s, 0xF, 0xF, false));
-            y[r] -= gis * xs;
-          }
-        }
-      };
-      static_for<kTile>(sub);
-      // A_IJ for phase 3
-      put_half(s_a, pa, J & 1, y);
-      // X^T_I as an A operand for the later tiles: element (row 4 lg + r,
-      // column lr) goes to lane (4 lg + r) + 16 (lr / 4), slot lr % 4
-      if (I + 1 < nt) {
-        bf16x4 hi, lo;
-        split4_bf16(y, hi, lo);
-        unsigned char* xs = s_xs;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = 4 * lg + r + 16 * (lr >> 2);
-          *reinterpret_cast<__bf16*>(xs + t * 8 + (lr & 3) * 2) = hi[r];
-          *reinterpret_cast<__bf16*>(xs + 512 + t * 8 + (lr & 3) * 2) = lo[r];
-        }
-        const bf16x4 th = *reinterpret_cast<const bf16x4*>(xs + lane * 8);
-        const bf16x4 tl = *reinterpret_cast<const bf16x4*>(xs + 512 + lane * 8);
-        if constexpr ((I & 1) == 0) {
-          xph[I / 2] = bf16x8{th[0], th[1], th[2], th[3], xph[I / 2][4], xph[I / 2][5], xph[I / 2][6], xph[I / 2][7]};
-          xpl[I / 2] = bf16x8{tl[0], tl[1], tl[2], tl[3], xpl[I / 2][4], xpl[I / 2][5], xpl[I / 2][6], xpl[I / 2][7]};
-        } else {
-          xph[I / 2] = bf16x8{xph[I / 2][0], xph[I / 2][1], xph[I / 2][2], xph[I / 2][3], th[0], th[1], th[2], th[3]};
-          xpl[I / 2] = bf16x8{xpl[I / 2][0], xpl[I / 2][1], xpl[I / 2][2], xpl[I / 2][3], tl[0], tl[1], tl[2], tl[3]};
-        }
-      }
+      bf16x4 yh, yl;
+      split4_bf16(y, yh, yl);
+      f32x4 x = mfma16k(ah, yh, f32x4{0.f, 0.f, 0.f, 0.f});
+      f32x4 x2 = mfma16k(al, yh, f32x4{0.f, 0.f, 0.f, 0.f});
+      x = mfma16k(ah, yl, x);
+      x += x2;
+      store_a(pa, J & 1, x);   // A_IJ for phase 3
+      if (I + 1 < nt) set_half(xph[I / 2], xpl[I / 2], I & 1, x);
     };
     static_for<NTM>(step_tile);
   }

@@ -91,7 +91,7 @@ __host__ __device__ inline int gla_large_buf(int D, int tm, int W) {
 }
 
 template <int D, int W, int BUF>
-__global__ __launch_bounds__(64 * gla_large_waves(D)) void verify_gla_large_kernel(VerifyArgs a) {
+__global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_waves_per_eu(2, 2))) void verify_gla_large_kernel(VerifyArgs a) {
   constexpr int NW = gla_large_waves(D);
   constexpr int NT = 64 * NW;
   constexpr int VT = D / kTile;            // value tiles: wave w < VT owns rows 16w..16w+15
