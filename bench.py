@@ -74,7 +74,8 @@ def conv_bytes(cfg, N, B, width):
 HASHED_SOURCES = ["include/treelin.h"] + [
     "paper_2608_01651_amd/csrc/" + f for f in
     ("tl_device.h", "tl_kernels.h", "verify_common.h", "verify_gdn.h", "verify_gla_small.h",
-     "verify_vector.h", "verify.hip", "verify_tiled.hip", "verify_gdn_dense.hip", "commit.hip")]
+     "verify_vector.h", "verify.hip", "verify_tiled.hip", "verify_gla_large.hip", "verify_gdn_dense.hip",
+     "commit.hip")]
 
 
 def source_hash():
