@@ -186,7 +186,7 @@ tl_status launch_verify_tiled(const tl_problem& p, const VerifyArgs& a, hipStrea
 tl_status launch_verify_gdn_dense(const tl_problem& p, const VerifyArgs& a, hipStream_t stream);
 tl_status launch_verify_gla_large(const tl_problem& p, const VerifyArgs& a, hipStream_t stream);
 int verify_gla_large_lds_bytes(int d, int tm);
-int verify_tiled_lds_bytes(int mode, int d, int tm, int W);
+int verify_tiled_lds_bytes(int d, int tm, int W);
 tl_status launch_commit(const tl_problem& p, const CommitArgs& a, hipStream_t stream);
 tl_status launch_commit_layers(const tl_problem& p, const CommitLayersArgs& a, hipStream_t stream);
 tl_status launch_accepted_path(const PathArgs& a, hipStream_t stream);

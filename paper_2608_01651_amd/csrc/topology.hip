@@ -107,7 +107,7 @@ tl_status launch_topology(const tl_problem& p, const TopoArgs& a, hipStream_t st
   if (mfma && p.mode == TL_MODE_GLA && tm <= 64)
     return (p.num_v_heads / p.num_qk_heads) % 2 == 0 ? launch_topo<kTopoWaveN, 1, 2>(a, stream)
                                                      : launch_topo<kTopoWaveN, 1, 1>(a, stream);
-  if (mfma && p.mode == TL_MODE_GDN && verify_tiled_lds_bytes(p.mode, p.d_k, tm, W) > 160 * 1024)
+  if (mfma && p.mode == TL_MODE_GDN && verify_tiled_lds_bytes(p.d_k, tm, W) > 160 * 1024)
     return launch_topo<kTopoGdn, 4>(a, stream);
   switch (W) {
     case 1: return launch_topo<kTopoLds, 1>(a, stream);

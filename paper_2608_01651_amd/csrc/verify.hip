@@ -35,10 +35,13 @@
 // steps with vector ALU products.
 //
 // Files: verify_gla_small.h (gated linear attention on MFMA, trees of <= 64
-// nodes), verify_tiled.hip (its own kernel: gated linear attention over
-// larger trees and the delta rule, node tile by node tile), verify_gdn.h (the
-// delta rule's per-wave MFMA path, for shapes whose tile-by-tile layout does
-// not fit in LDS), verify_vector.h (vector path), verify_common.h (layouts).
+// nodes), verify_gla_large.hip (its own kernel: gated linear attention over
+// trees of 65..256 nodes), verify_gdn_dense.hip (its own kernel: the delta
+// rule at d = 128 over node caps of up to 128), verify_tiled.hip (its own
+// kernel: the delta rule node tile by node tile, where that layout fits in
+// LDS), verify_gdn.h (the delta rule's per-wave MFMA path, for shapes whose
+// tile-by-tile layout does not fit in LDS), verify_vector.h (vector path),
+// verify_common.h (layouts).
 #include <hip/hip_runtime.h>
 
 #include "tl_device.h"
@@ -89,7 +92,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NH == 
   if constexpr (CAN_MFMA) {
     if (u.T >= kTile) {
       if constexpr (MODE == TL_MODE_GLA) {
-        static_assert(W == 1, "larger trees of gated linear attention run in the tiled kernel");
+        static_assert(W == 1, "larger trees of gated linear attention run in the large-tree kernel");
         verify_gla_small<D, BV, NH>(a, u);
       } else {
         verify_gdn_mfma<MODE, D, BV, W>(a, u);
@@ -150,7 +153,7 @@ static tl_status dispatch_w(const VerifyArgs& a, hipStream_t stream) {
   if constexpr (F32IN) {
     return launch_one<MODE, D, BV, F32IN, 4, 1>(a, stream);
   } else if constexpr (MODE == TL_MODE_GLA && D >= 32) {
-    // trees of more than 64 nodes are served by the tiled kernel
+    // trees of more than 64 nodes are served by the large-tree kernel
     if (a.tm > 64) return TL_EUNSUPPORTED;
     if ((a.Hv / a.Hk) % 2 == 0) return launch_one<MODE, D, BV, F32IN, 1, 2>(a, stream);
     return launch_one<MODE, D, BV, F32IN, 1, 1>(a, stream);
@@ -187,7 +190,7 @@ tl_status launch_verify(const tl_problem& p, const VerifyArgs& a, hipStream_t st
   if (p.in_dtype == TL_BF16 && p.d_k >= 32) {
     if (p.mode == TL_MODE_GLA && a.tm > 64) return launch_verify_gla_large(p, a, stream);
     const int W = a.tm > 128 ? 4 : (a.tm > 64 ? 2 : 1);
-    if (p.mode == TL_MODE_GDN && verify_tiled_lds_bytes(p.mode, p.d_k, a.tm, W) <= 160 * 1024)
+    if (p.mode == TL_MODE_GDN && verify_tiled_lds_bytes(p.d_k, a.tm, W) <= 160 * 1024)
       return launch_verify_tiled(p, a, stream);
   }
   if (p.mode == TL_MODE_GLA)

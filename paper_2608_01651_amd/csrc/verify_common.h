@@ -63,12 +63,6 @@ struct Unit {
   int b, h, hq, slice, off, T, sidx, tm;
 };
 
-// V^T (or U^T) row stride (elements) of the tiled kernel: the value term
-// reads whole 32-node chunks, so rows hold 32 * ceil(tm / 32) columns, plus 8:
-// stride / 2 = 4 (mod 8) 32-bit words, so the 8-byte fragment reads of 16 rows
-// by 4 lane groups hit 64 different banks.
-__host__ __device__ constexpr int gla_vt_stride(int tm) { return ((tm + 31) & ~31) + 8; }
-
 // C operand fragments of a tree of nt node tiles (trees of <= 64 nodes): tile
 // I uses I / 2 + 1 chunks of 32 ancestor columns.
 __host__ __device__ constexpr int gla_small_slots(int nt) { return (nt * nt + 2 * nt + (nt & 1)) / 4; }

@@ -1,5 +1,6 @@
-// Verify on MFMA, node tile by node tile: gated linear attention over trees
-// of 65..256 nodes and the delta rule over trees of up to 128 nodes.
+// Verify on MFMA, node tile by node tile: the gated delta rule wherever its
+// tile-sequential layout fits in LDS and the dense kernel does not serve it
+// (node caps of 129..160 at d = 128, and d = 32, 64).
 //
 // One workgroup per (request, v-head) with one wave per 16-row value tile
 // of the stored state (8 waves at d = 128).  Nodes are taken in tiles of 16
@@ -24,13 +25,12 @@
 //     bf16 hi + lo.  Only the wave's own rows of U^T are ever read back, so
 //     the solve needs no barrier: (I + G) is unit lower triangular and the
 //     tiles are solved in order (Lemma 3 bounds the depth, not needed here).
-//  3. readout: O^T = q_scale P_i (S Q_I^T) + U^T C^T (U = V for gated linear
-//     attention), stored as fp32.
+//  3. readout: O^T = q_scale P_i (S Q_I^T) + U^T C^T, stored as fp32.
 //
 // When LDS holds two chunk buffers, the coefficients of tile I + 1 are
 // formed while tile I's value work runs, with one barrier per tile;
 // otherwise the two phases alternate, with two.  The barriers order LDS
-// only, so the Q (and V) rows, loaded two tiles ahead, and the output
+// only, so the Q and V rows, loaded two tiles ahead, and the output
 // stores of the previous tile stay in flight across them.  The state is read
 // once, split into bf16 hi + lo in registers.
 #include <hip/hip_runtime.h>
@@ -47,46 +47,46 @@ struct TiledLayout {
   int cl, beta, mask, tmask, tin, gin, kst, frag, fragsz, frag2, ut, total;
 };
 
+// U^T row stride (elements): the value term reads whole 32-node chunks, so
+// rows hold 32 * ceil(tm / 32) columns, plus 8: stride / 2 = 4 (mod 8)
+// 32-bit words, so the 8-byte fragment reads of 16 rows by 4 lane groups hit
+// 64 different banks.
+__host__ __device__ constexpr int tiled_ut_stride(int tm) { return ((tm + 31) & ~31) + 8; }
+
 // LDS layout (bytes); identical on host and device.  With db the chunk
 // operands (and the in-tile block of G) are double-buffered.
-__host__ __device__ inline TiledLayout tiled_layout(int mode, int D, int tm, int W, bool db) {
-  const bool gdn = (mode == TL_MODE_GDN);
+__host__ __device__ inline TiledLayout tiled_layout(int D, int tm, int W, bool db) {
   const int nb = db ? 2 : 1;
   TiledLayout L;
   int o = 0;
   L.cl = o;    o += align16((tm + 32) * 4);                 // cumulative log2-decay (+1 chunk pad)
-  L.beta = o;  o += gdn ? align16(tm * 4) : 0;
+  L.beta = o;  o += align16(tm * 4);
   L.mask = o;  o += tm * W * 8;                             // M+ rows
   L.tmask = o; o += align16((tm / kTile) * W * 8);          // OR of M+ rows per node tile
   L.tin = o;   o += align16((tm / kTile) * 4);              // in-tile strict ancestors per tile
-  L.gin = o;   o += gdn ? nb * kTile * kTile * 4 : 0;       // in-tile block of G, row-major
+  L.gin = o;   o += nb * kTile * kTile * 4;                 // in-tile block of G, row-major
   L.kst = o;   o += tm * D * 2;                             // K rows, swizzled bf16
   L.frag = o;                                               // chunk operands | topology scratch
-  L.fragsz = ((tm + 31) / 32) * (gdn ? 4 : 2) * 1024;       // chunks of tiles 0..I, I < tm / 16
-  // gated linear attention keeps V^T in registers once it is staged, so its
-  // second chunk buffer reuses the V^T region
-  const bool alias = !gdn && db && D * gla_vt_stride(tm) * 2 >= L.fragsz;
+  L.fragsz = ((tm + 31) / 32) * 4 * 1024;                  // chunks of tiles 0..I, I < tm / 16
   {
-    const int fr = (alias ? 1 : nb) * L.fragsz;
+    const int fr = nb * L.fragsz;
     const int topo = kThreads * (4 + 4 + 4) + kThreads * W * 8;
     o += align16(fr > topo ? fr : topo);
   }
-  L.ut = o;    o += D * gla_vt_stride(tm) * 2 * (gdn ? 2 : 1);   // V^T, or U^T hi and lo
-  L.frag2 = !db ? L.frag : (alias ? L.ut : L.frag + L.fragsz);   // the second chunk buffer
+  L.ut = o;    o += D * tiled_ut_stride(tm) * 2 * 2;        // U^T hi and lo
+  L.frag2 = db ? L.frag + L.fragsz : L.frag;                // the second chunk buffer
   L.total = o;
   return L;
 }
 
-template <int MODE, int D, int W, bool DB>
+template <int D, int W, bool DB>
 __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(VerifyArgs a) {
   constexpr int NW = tiled_waves(D);
   constexpr int NT = 64 * NW;
   constexpr int VT = D / kTile;            // value tiles: wave w < VT owns rows 16w..16w+15
   constexpr int KS = D / 32;
   constexpr int CPRK = D / 8;
-  constexpr int VCH = D / 8;
-  constexpr bool GDN = (MODE == TL_MODE_GDN);
-  constexpr int NF = GDN ? 4 : 2;          // 1 KB operand pieces per chunk: C hi, C lo (G hi, G lo)
+  constexpr int NF = 4;                    // 1 KB operand pieces per chunk: C hi, C lo, G hi, G lo
   constexpr float kLog2e = 1.4426950408889634f;
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -113,8 +113,8 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     return;
   }
   const int tm = a.tm;
-  const int TS = gla_vt_stride(tm);
-  const TiledLayout L = tiled_layout(MODE, D, tm, W, DB);
+  const int TS = tiled_ut_stride(tm);
+  const TiledLayout L = tiled_layout(D, tm, W, DB);
   float* s_cl = reinterpret_cast<float*>(tl_lds + L.cl);
   float* s_beta = reinterpret_cast<float*>(tl_lds + L.beta);
   uint64_t* s_mask = reinterpret_cast<uint64_t*>(tl_lds + L.mask);
@@ -123,7 +123,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
   float* s_gin = reinterpret_cast<float*>(tl_lds + L.gin);
   __bf16* s_k = reinterpret_cast<__bf16*>(tl_lds + L.kst);
   unsigned char* s_frag = tl_lds + L.frag;
-  __bf16* s_ut = reinterpret_cast<__bf16*>(tl_lds + L.ut);          // V^T, or U^T hi
+  __bf16* s_ut = reinterpret_cast<__bf16*>(tl_lds + L.ut);          // U^T hi
   __bf16* s_utl = s_ut + D * TS;                                      // U^T lo
 
   const size_t qk_row = (size_t)a.Hk * D, v_row = (size_t)a.Hv * D;
@@ -131,14 +131,14 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
   const __bf16* Kb = reinterpret_cast<const __bf16*>(a.k) + (size_t)off * qk_row + (size_t)hq * D;
   const __bf16* Vb = reinterpret_cast<const __bf16*>(a.v) + (size_t)off * v_row + (size_t)h * D;
 
-  // ---- prologue: parents and gates, the wave's state rows, K into LDS, V^T
+  // ---- prologue: parents and gates, the wave's state rows, K into LDS
   TL_TRACE_POINT(a, 1);
   int par = -1;
   float gx = 0.f, bx = 0.f;
   if (tid < T) {
     par = a.parent[off + tid];
     gx = a.g[(size_t)(off + tid) * a.Hv + h];
-    if constexpr (GDN) bx = a.beta[(size_t)(off + tid) * a.Hv + h];
+    bx = a.beta[(size_t)(off + tid) * a.Hv + h];
   }
   f32x4 sraw[KS][2];
   if (vw) {
@@ -156,43 +156,9 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
       copy16_to_lds_async(Kb + (size_t)r * qk_row + c * 8, s_k + (size_t)base * 8);
     }
   }
-  const int npair = (T + 1) >> 1;
-  if constexpr (!GDN) {
-    // V rows -> V^T [D][TS] (two nodes per 32-bit word); task x = (chunk x / 128, pair x % 128)
-    constexpr int VTN = (128 * VCH + NT - 1) / NT;
-    bf16x8 v0[VTN], v1[VTN];
-#pragma unroll
-    for (int k = 0; k < VTN; ++k) {
-      const int x = tid + k * NT;
-      // loaded unconditionally from clamped rows (a load under a branch is
-      // waited for where the branch ends); tasks out of range store nothing
-      const int p = min(x & 127, npair - 1), cc = min(x >> 7, VCH - 1);
-      v0[k] = *reinterpret_cast<const bf16x8*>(Vb + (size_t)(2 * p) * v_row + cc * 8);
-      v1[k] = *reinterpret_cast<const bf16x8*>(Vb + (size_t)min(2 * p + 1, T - 1) * v_row + cc * 8);
-    }
-#pragma unroll
-    for (int k = 0; k < VTN; ++k) {
-      const int x = tid + k * NT;
-      const int p = x & 127, cc = x >> 7;
-      if (cc < VCH && p < npair) {
-        const bf16x8 odd = 2 * p + 1 < T ? v1[k] : bf16x8{};   // node 2p + 1, or zero past T
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          *reinterpret_cast<bf16x2*>(s_ut + (cc * 8 + e) * TS + 2 * p) = bf16x2{v0[k][e], odd[e]};
-      }
-    }
-    // columns 2*npair .. 32*ceil(T/32)-1 are read by the last chunk: zero
-    const int c0 = 2 * npair, c1 = (T + 31) & ~31;
-    const int nw = (c1 - c0) >> 1;
-    if (nw > 0) {
-      for (int x = tid; x < D * 16; x += NT) {
-        const int v = x >> 4, w2 = x & 15;
-        if (w2 < nw) *reinterpret_cast<uint32_t*>(s_ut + v * TS + c0 + 2 * w2) = 0u;
-      }
-    }
-  } else {
-    // U^T hi and lo start at zero: columns of later tiles are read (times zero
-    // coefficients) before they are written
+  // U^T hi and lo start at zero: columns of later tiles are read (times zero
+  // coefficients) before they are written
+  {
     const int words = (D * TS * 2 * 2) / 16;
     for (int x = tid; x < words; x += NT) reinterpret_cast<uint4*>(s_ut)[x] = uint4{0u, 0u, 0u, 0u};
   }
@@ -218,7 +184,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     __syncthreads();   // topology scratch is dead from here
     if (tid < T) {
       s_cl[tid] = cl * kLog2e;
-      if constexpr (GDN) s_beta[tid] = bx;
+      s_beta[tid] = bx;
       const int I = tid / kTile;
 #pragma unroll
       for (int w = 0; w < W; ++w) {
@@ -236,7 +202,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     }
   }
   wait_vmem();
-  __syncthreads();   // K, V^T / U^T, masks and decays are in LDS
+  __syncthreads();   // K, U^T, masks and decays are in LDS
   TL_TRACE_POINT(a, 3);
 
   // the wave's state rows, split into bf16 hi + lo MFMA A operands
@@ -256,7 +222,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     const bf16x4 x1 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + 2 + (lg >> 1)) ^ key) * 16));
     return bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
   };
-  // A-operand fragment of V^T / U^T row (16 w + lr), node chunk c
+  // A-operand fragment of U^T row (16 w + lr), node chunk c
   const int uo = ((kTile * wave + lr) * TS + 4 * lg) * 2;
   auto ufrag = [&](const __bf16* base, int c) {
     const unsigned char* p = reinterpret_cast<const unsigned char*>(base) + uo + 64 * c;
@@ -264,17 +230,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     const bf16x4 x1 = *reinterpret_cast<const bf16x4*>(p + 32);
     return bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
   };
-  // gated linear attention: the wave's V^T rows of every chunk, read once
-  // into registers (the V^T region then serves as the second chunk buffer;
-  // the barrier after the first chunks orders these reads before its use)
-  constexpr int NCH = GDN ? 1 : 2 * W;   // 32-node chunks of the largest tree
-  bf16x8 vreg[NCH];
-  if constexpr (!GDN) {
-    const int nch = (tm + 31) / 32;   // chunks that exist (uniform)
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) vreg[c] = (vw && c < nch) ? ufrag(s_ut, c) : bf16x8{};
-  }
-  // chunk operands: [chunk][piece][lane] 16 bytes, pieces C hi, C lo (, -G hi, -G lo)
+  // chunk operands: [chunk][piece][lane] 16 bytes, pieces C hi, C lo, -G hi, -G lo
 
   // ---- node tiles
   const int nt = (T + kTile - 1) / kTile;
@@ -295,7 +251,6 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     }
   };
   auto load_v = [&](int I) {
-    if constexpr (!GDN) return bf16x4{};
     const int r = min(kTile * I + lr, T - 1);
     const int col = min(kTile * wave, D - kTile) + 4 * lg;   // waves without value rows read a valid column
     return *reinterpret_cast<const bf16x4*>(Vb + (size_t)r * v_row + col);
@@ -312,12 +267,8 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     const bool iv = i < T;
     const float cv = s_cl[i];
     t.cli = iv ? cv : 0.f;
-    if constexpr (GDN) {
-      const float bv = s_beta[min(i, tm - 1)];
-      t.bi = iv ? bv : 0.f;
-    } else {
-      t.bi = 0.f;
-    }
+    const float bv = s_beta[min(i, tm - 1)];
+    t.bi = iv ? bv : 0.f;
   };
   // 32 bits of tile I's OR mask starting at node 32 c (uniform)
   auto tile_bits32 = [&](int I, int c) __attribute__((always_inline)) {
@@ -340,7 +291,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           kj[ks] = kfrag(kTile * J, ks);
-          if constexpr (GDN) kfi[ks] = kfrag(kTile * I, ks);
+          kfi[ks] = kfrag(kTile * I, ks);
         }
         const uint64_t mw = (i < T) ? s_mask[i * W + (J >> 2)] : 0ull;   // M+ row of node i
         const f32x4 clj = *reinterpret_cast<const f32x4*>(s_cl + kTile * J + 4 * lg);
@@ -348,7 +299,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           qk = mfma16(kj[ks], qf[ks], qk);               // rows j, column i: k_j . q_i
-          if constexpr (GDN) kk = mfma16(kj[ks], kfi[ks], kk);
+          kk = mfma16(kj[ks], kfi[ks], kk);
         }
         const unsigned mb = (unsigned)(mw >> ((J & 3) * kTile + 4 * lg)) & 0xFu;
         const unsigned self = (J == I) ? (1u << lr) >> (4 * lg) : 0u;   // bit r: j == i
@@ -357,15 +308,13 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
           const bool m = (mb >> r) & 1u;
           const float dec = __builtin_amdgcn_exp2f(t.cli - clj[r]);
           cv[r] = m ? (dec * a.q_scale) * qk[r] : 0.f;
-          if constexpr (GDN) gv[r] = (m && !((self >> r) & 1u)) ? (t.bi * dec) * kk[r] : 0.f;
+          gv[r] = (m && !((self >> r) & 1u)) ? (t.bi * dec) * kk[r] : 0.f;
         }
       }
-      if constexpr (GDN) {
-        if (J == I) {   // the in-tile block: row-major to LDS, zero in the operand
-          *reinterpret_cast<f32x4*>(gin + lr * kTile + 4 * lg) = f32x4{gv[0], gv[1], gv[2], gv[3]};
+      if (J == I) {   // the in-tile block: row-major to LDS, zero in the operand
+        *reinterpret_cast<f32x4*>(gin + lr * kTile + 4 * lg) = f32x4{gv[0], gv[1], gv[2], gv[3]};
 #pragma unroll
-          for (int r = 0; r < 4; ++r) gv[r] = 0.f;
-        }
+        for (int r = 0; r < 4; ++r) gv[r] = 0.f;
       }
       // this half's 8 bytes of each 16-byte operand piece: hi01 hi23, then lo01 lo23
       uint32_t cw[4], gw[4];
@@ -374,12 +323,11 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
       unsigned char* pc = buf + ((c * NF) * 64 + lane) * 16 + hf * 8;
       *reinterpret_cast<uint2*>(pc) = uint2{cw[0], cw[1]};
       *reinterpret_cast<uint2*>(pc + 1024) = uint2{cw[2], cw[3]};
-      if constexpr (GDN) {   // stored negated: U^T (-G)^T is subtracted by accumulation
-        split2_bf16(-gv[0], -gv[1], gw[0], gw[2]);
-        split2_bf16(-gv[2], -gv[3], gw[1], gw[3]);
-        *reinterpret_cast<uint2*>(pc + 2048) = uint2{gw[0], gw[1]};
-        *reinterpret_cast<uint2*>(pc + 3072) = uint2{gw[2], gw[3]};
-      }
+      // G stored negated: U^T (-G)^T is subtracted by accumulation
+      split2_bf16(-gv[0], -gv[1], gw[0], gw[2]);
+      split2_bf16(-gv[2], -gv[3], gw[1], gw[3]);
+      *reinterpret_cast<uint2*>(pc + 2048) = uint2{gw[0], gw[1]};
+      *reinterpret_cast<uint2*>(pc + 3072) = uint2{gw[2], gw[3]};
     }
   };
 
@@ -391,9 +339,9 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
   struct ChunkOps {
     bf16x8 ch, cl, gh, gl, uh, ul;
   };
-  // delta rule: U^T of every completed chunk (both of its tiles solved),
-  // this wave's rows, kept in registers once read back
-  constexpr int NCU = GDN ? 2 * W : 1;
+  // U^T of every completed chunk (both of its tiles solved), this wave's
+  // rows, kept in registers once read back
+  constexpr int NCU = 2 * W;
   bf16x8 ureg_h[NCU], ureg_l[NCU];
   auto value_work = [&](int I, const bf16x8 (&qf)[KS], const bf16x4 vcur, const TileIn& t,
                         const unsigned char* buf, const float* gin) __attribute__((always_inline)) {
@@ -405,11 +353,9 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
       o.ch = *reinterpret_cast<const bf16x8*>(pc(c, 0));
       o.cl = *reinterpret_cast<const bf16x8*>(pc(c, 1));
       o.uh = ufrag(s_ut, c);
-      if constexpr (GDN) {
-        o.gh = *reinterpret_cast<const bf16x8*>(pc(c, 2));
-        o.gl = *reinterpret_cast<const bf16x8*>(pc(c, 3));
-        o.ul = ufrag(s_utl, c);
-      }
+      o.gh = *reinterpret_cast<const bf16x8*>(pc(c, 2));
+      o.gl = *reinterpret_cast<const bf16x8*>(pc(c, 3));
+      o.ul = ufrag(s_utl, c);
     };
     // chunks with an ancestor of tile I (uniform)
     uint32_t live = 0;
@@ -417,24 +363,20 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     for (int c = 0; c < 2 * W; ++c) live |= (tile_bits32(I, c) != 0u ? 1u : 0u) << c;
     live = __builtin_amdgcn_readfirstlane(live);
     f32x4 x = f32x4{0.f, 0.f, 0.f, 0.f}, acc = x, acc2 = x;
-    // B0^T = S Q_I^T (and S K_I^T for the delta rule), independent of the chunks
+    // B0^T = S Q_I^T and S K_I^T, independent of the chunks
     f32x4 b0 = f32x4{0.f, 0.f, 0.f, 0.f}, sk = b0;
     bf16x8 kfi[KS];
-    if constexpr (GDN) {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kfi[ks] = kfrag(kTile * I, ks);
-    }
+    for (int ks = 0; ks < KS; ++ks) kfi[ks] = kfrag(kTile * I, ks);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       b0 = mfma16(shi[ks], qf[ks], b0);
       b0 = mfma16(slo[ks], qf[ks], b0);
-      if constexpr (GDN) {
-        sk = mfma16(shi[ks], kfi[ks], sk);
-        sk = mfma16(slo[ks], kfi[ks], sk);
-      }
+      sk = mfma16(shi[ks], kfi[ks], sk);
+      sk = mfma16(slo[ks], kfi[ks], sk);
     }
-    // the chunks of earlier tiles (for gated linear attention: all of them)
-    if constexpr (GDN) {
+    // the chunks of earlier tiles
+    {
 #pragma unroll
       for (int c = 0; c < NCU; ++c) {   // completed chunks: U^T from registers
         if (c >= cI || !((live >> c) & 1u)) continue;   // uniform
@@ -452,19 +394,10 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
         x = mfma16(o.ul, o.gh, x);
         acc = mfma16(o.ul, o.ch, acc);
       }
-    } else {
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) {   // V^T from registers: a static chunk index
-        if (c > cI || !((live >> c) & 1u)) continue;   // uniform
-        const bf16x8 ch = *reinterpret_cast<const bf16x8*>(pc(c, 0));
-        const bf16x8 cl = *reinterpret_cast<const bf16x8*>(pc(c, 1));
-        acc = mfma16(vreg[c], ch, acc);
-        acc = mfma16(vreg[c], cl, acc);
-      }
     }
     const float Pi = iv ? __builtin_amdgcn_exp2f(t.cli) : 0.f;
 
-    if constexpr (GDN) {
+    {
       // 2. U_I: X = beta (V - P S K^T) - U^T G^T over the earlier tiles (in x),
       // then the chunk of tile I: the G columns of tile I are zero there (its
       // block is solved below) and those of tile I - 1 are final
@@ -517,7 +450,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
         ureg_l[c] = here ? ul : ureg_l[c];
       }
     }
-    // 3. O^T = q_scale P_i B0^T + U^T C^T (U = V for gated linear attention)
+    // 3. O^T = q_scale P_i B0^T + U^T C^T
     const float ps = Pi * a.q_scale;
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc[r] = ps * b0[r] + (acc[r] + acc2[r]);
@@ -564,7 +497,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
       tile_in(I + 1, tn);
       chunks(I + 1, qb, tn, bufp(I + 1), ginp(I + 1));
     }
-    if (vw && pend_row >= 0) store_out<MODE == TL_MODE_GDN>(obase + (size_t)pend_row * v_row, pend);
+    if (vw && pend_row >= 0) store_out<true>(obase + (size_t)pend_row * v_row, pend);
     pend_row = -1;
     load_q(I + 2, qc);   // rows clamped: harmless past the last tile
     vc = load_v(I + 2);
@@ -591,24 +524,24 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     if (I + 1 < nt) tile_step(I + 1, q1, q2, q0, v1, v2, v0);
     if (I + 2 < nt) tile_step(I + 2, q2, q0, q1, v2, v0, v1);
   }
-  if (vw && pend_row >= 0) store_out<MODE == TL_MODE_GDN>(obase + (size_t)pend_row * v_row, pend);
+  if (vw && pend_row >= 0) store_out<true>(obase + (size_t)pend_row * v_row, pend);
   TL_TRACE_POINT(a, 15);
 }
 
-// LDS bytes of the tiled kernel for a problem (double-buffered if that fits).
-int verify_tiled_lds_bytes(int mode, int d, int tm, int W) {
-  const int db = tiled_layout(mode, d, tm, W, true).total;
-  return db <= 160 * 1024 ? db : tiled_layout(mode, d, tm, W, false).total;
+// LDS bytes of the tiled kernel for a node cap (double-buffered if that fits).
+int verify_tiled_lds_bytes(int d, int tm, int W) {
+  const int db = tiled_layout(d, tm, W, true).total;
+  return db <= 160 * 1024 ? db : tiled_layout(d, tm, W, false).total;
 }
 
-template <int MODE, int D, int W, bool DB>
+template <int D, int W, bool DB>
 static tl_status launch_tiled_one(const VerifyArgs& a, hipStream_t stream) {
-  const int lds = tiled_layout(MODE, D, a.tm, W, DB).total;
+  const int lds = tiled_layout(D, a.tm, W, DB).total;
   if (lds > 160 * 1024) return TL_EUNSUPPORTED;
   const long blocks = 8 * (((long)a.batch * a.Hk + 7) / 8) * (a.Hv / a.Hk);
   if (blocks == 0) return TL_OK;
   if (blocks > 0x7fffffffL) return TL_EINVAL;
-  auto kern = verify_tiled_kernel<MODE, D, W, DB>;
+  auto kern = verify_tiled_kernel<D, W, DB>;
   if (lds > 64 * 1024) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                             hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess)
@@ -620,25 +553,25 @@ static tl_status launch_tiled_one(const VerifyArgs& a, hipStream_t stream) {
   return hipGetLastError() == hipSuccess ? TL_OK : TL_EHIP;
 }
 
-template <int MODE, int D, int W>
+template <int D, int W>
 static tl_status launch_tiled_db(const VerifyArgs& a, hipStream_t stream) {
-  if (tiled_layout(MODE, D, a.tm, W, true).total <= 160 * 1024) return launch_tiled_one<MODE, D, W, true>(a, stream);
-  return launch_tiled_one<MODE, D, W, false>(a, stream);
+  if (tiled_layout(D, a.tm, W, true).total <= 160 * 1024) return launch_tiled_one<D, W, true>(a, stream);
+  return launch_tiled_one<D, W, false>(a, stream);
 }
 
-template <int MODE, int D>
+template <int D>
 static tl_status launch_tiled_w(const VerifyArgs& a, hipStream_t stream) {
-  if (a.tm > 128) return launch_tiled_db<MODE, D, 4>(a, stream);
-  if (a.tm > 64) return launch_tiled_db<MODE, D, 2>(a, stream);
-  return launch_tiled_db<MODE, D, 1>(a, stream);
+  if (a.tm > 128) return launch_tiled_db<D, 4>(a, stream);
+  if (a.tm > 64) return launch_tiled_db<D, 2>(a, stream);
+  return launch_tiled_db<D, 1>(a, stream);
 }
 
 tl_status launch_verify_tiled(const tl_problem& p, const VerifyArgs& a, hipStream_t stream) {
-  const bool gdn = p.mode == TL_MODE_GDN;
+  if (p.mode != TL_MODE_GDN) return TL_EUNSUPPORTED;
   switch (p.d_k) {
-    case 32: return gdn ? launch_tiled_w<TL_MODE_GDN, 32>(a, stream) : launch_tiled_w<TL_MODE_GLA, 32>(a, stream);
-    case 64: return gdn ? launch_tiled_w<TL_MODE_GDN, 64>(a, stream) : launch_tiled_w<TL_MODE_GLA, 64>(a, stream);
-    case 128: return gdn ? launch_tiled_w<TL_MODE_GDN, 128>(a, stream) : launch_tiled_w<TL_MODE_GLA, 128>(a, stream);
+    case 32: return launch_tiled_w<32>(a, stream);
+    case 64: return launch_tiled_w<64>(a, stream);
+    case 128: return launch_tiled_w<128>(a, stream);
     default: return TL_EUNSUPPORTED;
   }
 }
