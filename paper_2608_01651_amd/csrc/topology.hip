@@ -2,7 +2,7 @@
 // the notation table of §4.1, built once per request per round and reusable
 // across layers and heads (§4.3).  One workgroup per request.
 //
-// Every verify kernel builds the topology on chip with one of three
+// Every verify kernel builds the topology on chip with one of four
 // routines, and the export runs the routine that the verify kernel serving
 // the same problem runs, so that the bits it returns are the bits that
 // kernel masks its coefficients with:
@@ -17,7 +17,11 @@
 //               own pass counts depths without masks;
 //   kTopoGdn    the delta rule's kernel for node caps beyond the tile walk's
 //               LDS (d = 128, caps of 176..256): wave_topology for trees of
-//               <= 64 nodes, build_topology<4> above.
+//               <= 64 nodes, build_topology<4> above;
+//   kTopoWalk1  wave_topology_walk, one wavefront holding 64 W nodes
+//               (root-path walks in LDS, then pointer jumping, no workgroup
+//               barrier): the delta rule's dense kernel (bf16, d = 128, node
+//               caps of up to 128).
 // The depth of a node is its number of strict ancestors; where the routine
 // yields only the mask it is the mask's popcount minus one.
 #include <hip/hip_runtime.h>
@@ -28,7 +32,7 @@
 
 namespace tl {
 
-enum TopoKind { kTopoWaveN = 0, kTopoLds = 1, kTopoGdn = 2 };
+enum TopoKind { kTopoWaveN = 0, kTopoLds = 1, kTopoGdn = 2, kTopoWalk1 = 3 };
 
 template <int W>
 __device__ inline void store_topology(const TopoArgs& a, const Request& rq, int node, int dep,
@@ -51,6 +55,31 @@ __global__ __launch_bounds__(kThreads) void topology_kernel(TopoArgs a) {
   if (!load_request(a.node_offsets, blockIdx.x, a.max_nodes, a.dev_err, rq)) return;
   const int T = rq.T;
   if (T == 0) return;
+  if constexpr (KIND == kTopoWalk1) {
+    if (tid >= 64) return;   // one wavefront; the others take no part
+    int par[W];
+    float x[W], cl[W];
+    uint64_t msk[W][W];
+#pragma unroll
+    for (int e = 0; e < W; ++e) {   // lanes past the tree read its last node, as the kernel does
+      par[e] = a.parent[rq.off + min(tid + 64 * e, T - 1)];
+      x[e] = 0.f;
+    }
+    if (!wave_topology_walk<W, W>(par, x, T, s_jmp, s_acc, s_msk, cl, msk)) {
+      if (tid == 0) report(a.dev_err, TL_EBADTREE);
+      return;
+    }
+#pragma unroll
+    for (int e = 0; e < W; ++e) {
+      if (tid + 64 * e < T) {
+        int c = 0;
+#pragma unroll
+        for (int w = 0; w < W; ++w) c += __popcll(msk[e][w]);
+        store_topology<W>(a, rq, tid + 64 * e, c - 1, msk[e]);
+      }
+    }
+    return;
+  }
   const bool wave_path = KIND == kTopoWaveN || (KIND == kTopoGdn && T <= 64);
   if (wave_path) {
     if (tid >= 64) return;   // one wavefront; the others take no part
@@ -104,6 +133,8 @@ tl_status launch_topology(const tl_problem& p, const TopoArgs& a, hipStream_t st
   const int tm = (p.max_nodes + 15) & ~15;
   const int W = tm > 128 ? 4 : (tm > 64 ? 2 : 1);
   const bool mfma = p.in_dtype == TL_BF16 && p.d_k >= 32;
+  if (mfma && p.mode == TL_MODE_GDN && p.d_k == 128 && tm <= 128)
+    return W == 1 ? launch_topo<kTopoWalk1, 1>(a, stream) : launch_topo<kTopoWalk1, 2>(a, stream);
   if (mfma && p.mode == TL_MODE_GLA && tm <= 64)
     return (p.num_v_heads / p.num_qk_heads) % 2 == 0 ? launch_topo<kTopoWaveN, 1, 2>(a, stream)
                                                      : launch_topo<kTopoWaveN, 1, 1>(a, stream);

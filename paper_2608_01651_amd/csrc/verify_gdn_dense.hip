@@ -15,7 +15,9 @@
 //
 // The node-by-node coupling sits in A = (I + G)^{-1}, a T x T matrix that does
 // not depend on the value channels.  So one workgroup of 8 wave64s per
-// (request, v-head) runs three phases separated by two barriers:
+// (request, v-head) runs three phases separated by two barriers, after a
+// prologue in which wave 0 forms the topology alone (wave_topology_walk, no
+// workgroup barrier) while waves 1..7 issue the K, Q and V copies:
 //  1. every wave forms its share of the 16 x 16 blocks (I, J <= I) of C and G
 //     (K_J Q_I^T and K_J K_I^T on MFMA, masked by the M+ rows, decayed) into
 //     LDS in MFMA operand order, and of the in-tile inverses (I + G_II)^{-1}
@@ -85,7 +87,7 @@ __host__ __device__ constexpr int gpair_row(int I) { return (I / 2) * (I / 2) + 
 }  // namespace
 
 struct DenseLayout {
-  int cl, beta, mask, tmask, tin, gin, kq, cst, gst, ainv, total;
+  int flag, cl, beta, mask, tmask, tin, gin, kq, cst, gst, ainv, total;
 };
 
 // LDS layout (bytes); identical on host and device.
@@ -93,6 +95,7 @@ __host__ __device__ inline DenseLayout dense_layout(int tm, int W) {
   const int nb = tm / kTile;
   DenseLayout L;
   int o = 0;
+  L.flag = o;  o += 16;                              // the tree is malformed
   L.cl = o;    o += align16((tm + 16) * 4);          // cumulative log2-decay
   L.beta = o;  o += align16(tm * 4);
   L.mask = o;  o += tm * W * 8;                      // M+ rows
@@ -175,26 +178,27 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   const __bf16* Kb = reinterpret_cast<const __bf16*>(a.k) + (size_t)off * qk_row + (size_t)hq * D;
   const __bf16* Vb = reinterpret_cast<const __bf16*>(a.v) + (size_t)off * v_row + (size_t)h * D;
 
-  // ---- prologue.  Loads in the order they are needed: parents and gates,
-  // K, Q and V rows (direct copies into swizzled LDS), then the wave's state
-  // rows (needed last, in phase 1b).
-  // The copies are issued by the waves past the tree's nodes (waves 2..7:
-  // threads >= 128 >= T), so the waves that hold nodes wait for their
-  // parents and gates alone before the topology: the compiler does not see
-  // the copies, and loads complete in issue order.
+  // ---- prologue.  Wave 0 loads the parents and gates and forms the
+  // topology alone (no workgroup barrier) while waves 1..7 issue the direct
+  // copies of the K, Q and V rows into swizzled LDS; every wave then loads
+  // its state rows (needed last, in phase 1b).  The copies are issued as
+  // inline assembly, which the compiler does not count, and loads complete
+  // in issue order.
   TL_TRACE_POINT(a, 1);
-  constexpr int kCopyWave0 = kDenseMaxTiles * kTile / 64;   // first wave without nodes
-  static_assert(kCopyWave0 < kDenseWaves, "some waves hold no node");
-  int par = -1;
-  float gx = 0.f, bx = 0.f;
-  if (tid < T) {
-    par = a.parent[off + tid];
-    gx = a.g[(size_t)(off + tid) * a.Hv + h];
-    bx = a.beta[(size_t)(off + tid) * a.Hv + h];
-  }
-  if (wave >= kCopyWave0) {   // uniform
-    constexpr int CT = kDenseThreads - 64 * kCopyWave0;
-    for (int base = (wave - kCopyWave0) * 64; base < T * CPRK; base += CT) {
+  constexpr int NE = W;   // nodes per lane of wave 0 (node cap <= 64 W)
+  int par[NE];
+  float gx[NE], bx[NE];
+  if (wave == 0) {   // uniform
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {   // unconditional loads, clamped to the tree
+      const int i = off + min(lane + 64 * e, T - 1);
+      par[e] = a.parent[i];
+      gx[e] = a.g[(size_t)i * a.Hv + h];
+      bx[e] = a.beta[(size_t)i * a.Hv + h];
+    }
+  } else {
+    constexpr int CT = kDenseThreads - 64;
+    for (int base = (wave - 1) * 64; base < T * CPRK; base += CT) {
       const int p = base + lane;
       if (p < T * CPRK) {
         const int r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
@@ -204,9 +208,10 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
     }
     // the V rows of every node tile, into the C region (rows past T repeat
     // row T - 1; their R entries are set to zero)
-    for (int base = (wave - kCopyWave0) * 64; base < kTile * nt * CPRK; base += CT) {   // multiple of 64
+    for (int base = (wave - 1) * 64; base < kTile * nt * CPRK; base += CT) {
       const int p = base + lane, r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
-      copy16_to_lds_async(Vb + (size_t)min(r, T - 1) * v_row + c * 8, s_v + (size_t)base * 8);
+      if (p < kTile * nt * CPRK)
+        copy16_to_lds_async(Vb + (size_t)min(r, T - 1) * v_row + c * 8, s_v + (size_t)base * 8);
     }
   }
   TL_TRACE_POINT(a, 6);
@@ -222,41 +227,41 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
     }
   }
 
-  // ---- topology: M+ rows, cumulative log-decay, per-tile masks
+  // ---- topology, by wave 0: M+ rows, cumulative log-decay, per-tile masks
   TL_TRACE_POINT(a, 2);
-  for (int x = tid; x < (tm / kTile) * W; x += kDenseThreads) s_tmask[x] = 0;
-  for (int x = tid; x < tm / kTile; x += kDenseThreads) s_tin[x] = 0u;
-  {
+  int* s_flag = reinterpret_cast<int*>(tl_lds + L.flag);
+  if (wave == 0) {   // uniform
+    for (int x = lane; x < (tm / kTile) * W; x += 64) s_tmask[x] = 0;
+    for (int x = lane; x < tm / kTile; x += 64) s_tin[x] = 0u;
     int* s_jmp = reinterpret_cast<int*>(s_g);
-    float* s_acc = reinterpret_cast<float*>(s_jmp + kThreads);
-    int* s_cnt = reinterpret_cast<int*>(s_acc + kThreads);
-    uint64_t* s_msk = reinterpret_cast<uint64_t*>(s_cnt + kThreads);
-    int dep = 0;
-    float cl = 0.f;
-    uint64_t msk[W];
-    const bool ok = build_topology<W, true>(par, T, gx, s_jmp, s_acc, s_cnt, s_msk, dep, cl, msk);
-    if (!ok) {
-      if (tid == 0) report(a.dev_err, TL_EBADTREE);
-      wait_vmem();   // let the in-flight LDS copies land before the block retires
-      return;
+    float* s_acc = reinterpret_cast<float*>(s_jmp + 64 * NE);
+    uint64_t* s_msk = reinterpret_cast<uint64_t*>(s_acc + 64 * NE);
+    float cl[NE];
+    uint64_t msk[NE][W];
+    const bool ok = wave_topology_walk<W, NE>(par, gx, T, s_jmp, s_acc, s_msk, cl, msk);
+    if (lane == 0) {
+      *s_flag = ok ? 0 : 1;
+      if (!ok) report(a.dev_err, TL_EBADTREE);
     }
-    __syncthreads();   // topology scratch is dead from here
-    if (tid < T) {
-      s_cl[tid] = cl * kLog2e;
-      s_beta[tid] = bx;
-      const int I = tid / kTile;
+    if (ok) {   // uniform
 #pragma unroll
-      for (int w = 0; w < W; ++w) {
-        s_mask[tid * W + w] = msk[w];
-        if (msk[w]) atomicOr(reinterpret_cast<unsigned long long*>(&s_tmask[I * W + w]),
-                             (unsigned long long)msk[w]);
+      for (int e = 0; e < NE; ++e) {
+        const int i = lane + 64 * e;
+        if (i < T) {
+          s_cl[i] = cl[e] * kLog2e;
+          s_beta[i] = bx[e];
+          const int I = i / kTile;
+#pragma unroll
+          for (int w = 0; w < W; ++w) {
+            s_mask[i * W + w] = msk[e][w];
+            if (msk[e][w]) atomicOr(reinterpret_cast<unsigned long long*>(&s_tmask[I * W + w]),
+                                    (unsigned long long)msk[e][w]);
+          }
+          // node i's ancestors inside its tile: bits (I % 4) 16 .. + 15 of word e
+          const uint32_t in_tile = (uint32_t)(msk[e][e] >> ((I & 3) * kTile)) & 0xFFFFu & ~(1u << (i & 15));
+          if (in_tile) atomicOr(&s_tin[I], in_tile);
+        }
       }
-      uint64_t wv = msk[0];
-#pragma unroll
-      for (int w = 1; w < W; ++w)
-        if ((tid >> 6) == w) wv = msk[w];
-      const uint32_t in_tile = (uint32_t)(wv >> ((I & 3) * kTile)) & 0xFFFFu & ~(1u << (tid & 15));
-      if (in_tile) atomicOr(&s_tin[I], in_tile);
     }
   }
   TL_TRACE_POINT(a, 7);
@@ -264,6 +269,10 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   // at most the state loads of this wave are outstanding
   wait_vmem_below<2 * KS>();
   lds_barrier();   // K, Q, V, masks and decays are in LDS (the state stays in flight)
+  if (*s_flag) {   // uniform: a malformed tree (reported by wave 0)
+    wait_vmem();   // the state rows land before the block retires
+    return;
+  }
   // V[node 16 J + 4 lg + e][channel 16 wave + lr] by LDS transpose reads: lane
   // (lg, lr) names row 16 J + 4 lg + lr / 4 and channels 16 wave + 4 (lr % 4)
   // .. + 3, so it receives channel 16 wave + lr of nodes 16 J + 4 lg .. + 3
@@ -470,6 +479,7 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   bf16x8 shi[KS], slo[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) split8_bf16(sraw[ks][0], sraw[ks][1], shi[ks], slo[ks]);
+
   TL_TRACE_POINT(a, 9);
 #pragma unroll
   for (int I = 0; I < NTM; ++I) {
