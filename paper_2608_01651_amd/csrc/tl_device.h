@@ -252,14 +252,21 @@ __device__ inline bool build_topology(int par, int T, float x,
 // The same topology (cl and the M+ rows of build_topology) formed by one wave
 // alone, with no workgroup barrier, so that it can run while the other waves
 // of the workgroup are held up issuing their copies: lane l holds nodes
-// l + 64 e (e < NE), so T <= 64 NE.  The same steps: root-path walks through
-// the parents in LDS for at most kTopoWalk steps, then pointer jumping over
-// the walked segments.  The LDS accesses of one wave take effect in program
-// order, so no step needs a barrier.  Scratch: s_jmp and s_acc of 64 NE
-// entries, s_msk of W * 64 NE words.  Returns false (uniformly over the
-// wave) if a parent breaks the parent-before-child order.
+// l + 64 e (e < NE), so T <= 64 NE.  Pointer jumping: a node's state (cl,
+// mask) covers the path segment from itself up to (excluding) jmp; each
+// round every node publishes its state, then folds in the state published
+// at jmp, doubling its segment, so a tree of depth d takes ceil(log2(d + 1))
+// rounds.  The LDS accesses of one wave take effect in program order, so no
+// round needs a barrier (with one wave, rounds are cheaper than the
+// one-ancestor-per-step walks build_topology starts with).  Ancestors have
+// smaller indices, so the M+ row of node n has no bit in words above n / 64:
+// those words are not published, and a fold takes a word from jmp only if
+// jmp published it.  Scratch: s_jmp and s_acc of 64 NE entries, s_msk of
+// W * 64 NE words (word-major, so that a publish writes consecutive words).
+// Returns false (uniformly over the wave) if a parent breaks the
+// parent-before-child order.
 template <int W, int NE>
-__device__ inline bool wave_topology_walk(const int (&par)[NE], const float (&x)[NE], int T,
+__device__ inline bool wave_topology_jump(const int (&par)[NE], const float (&x)[NE], int T,
                                           int32_t* s_jmp, float* s_acc, uint64_t* s_msk,
                                           float (&cl)[NE], uint64_t (&mask)[NE][W]) {
   static_assert(NE <= W, "node l + 64 e has its bit in word e");
@@ -271,10 +278,6 @@ __device__ inline bool wave_topology_walk(const int (&par)[NE], const float (&x)
     const int i = lane + 64 * e;
     const bool live = i < T;
     bad |= live && !(par[e] == -1 || (par[e] >= 0 && par[e] < i));
-    if (live) {   // parents and own values, read by the walks of descendants
-      s_jmp[i] = par[e];
-      s_acc[i] = x[e];
-    }
     jmp[e] = live ? par[e] : -1;
     cl[e] = x[e];
 #pragma unroll
@@ -288,39 +291,27 @@ __device__ inline bool wave_topology_walk(const int (&par)[NE], const float (&x)
     for (int e = 0; e < NE; ++e) any |= jmp[e] >= 0;
     return __ballot(any) != 0ull;
   };
-  for (int s = 0; s < kTopoWalk && pending(); ++s) {
-#pragma unroll
-    for (int e = 0; e < NE; ++e) {
-      if (jmp[e] >= 0) {
-        const int j = jmp[e];
-        const int up = s_jmp[j];
-        cl[e] += s_acc[j];
-#pragma unroll
-        for (int w = 0; w < W; ++w) mask[e][w] |= ((j >> 6) == w) ? (1ull << (j & 63)) : 0ull;
-        jmp[e] = up;
-      }
-    }
-  }
-  // pointer jumping: each round every node publishes its segment (its state
-  // up to, excluding, jmp), then folds in the segment published at jmp
   while (pending()) {
 #pragma unroll
-    for (int e = 0; e < NE; ++e) {
+    for (int e = 0; e < NE; ++e) {   // publish
       const int i = lane + 64 * e;
       if (i < T) {
         s_jmp[i] = jmp[e];
         s_acc[i] = cl[e];
 #pragma unroll
-        for (int w = 0; w < W; ++w) s_msk[w * 64 * NE + i] = mask[e][w];
+        for (int w = 0; w <= e; ++w) s_msk[w * 64 * NE + i] = mask[e][w];
       }
     }
 #pragma unroll
-    for (int e = 0; e < NE; ++e) {
+    for (int e = 0; e < NE; ++e) {   // fold in the segment above
       if (jmp[e] >= 0) {
         const int j = jmp[e];
         cl[e] += s_acc[j];
 #pragma unroll
-        for (int w = 0; w < W; ++w) mask[e][w] |= s_msk[w * 64 * NE + j];
+        for (int w = 0; w <= e; ++w) {
+          const uint64_t m = s_msk[w * 64 * NE + j];   // in bounds; stale where w > j / 64
+          if (w <= (j >> 6)) mask[e][w] |= m;
+        }
         jmp[e] = s_jmp[j];
       }
     }

@@ -11,17 +11,17 @@
 //               (bf16, d >= 32), the small-tree MFMA kernel;
 //   kTopoLds    build_topology<W>, one thread per node: root-path walks
 //               through the parents in LDS, finished by pointer jumping for
-//               deep trees: the large-tree kernel of gated linear attention (caps
-//               of 65..256), the delta rule's tile walk (where its layout
+//               deep trees: the delta rule's tile walk (where its layout
 //               fits LDS), and the vector path (fp32 inputs or d = 16), whose
 //               own pass counts depths without masks;
 //   kTopoGdn    the delta rule's kernel for node caps beyond the tile walk's
 //               LDS (d = 128, caps of 176..256): wave_topology for trees of
 //               <= 64 nodes, build_topology<4> above;
-//   kTopoWalk1  wave_topology_walk, one wavefront holding 64 W nodes
-//               (root-path walks in LDS, then pointer jumping, no workgroup
-//               barrier): the delta rule's dense kernel (bf16, d = 128, node
-//               caps of up to 128).
+//   kTopoJump1  wave_topology_jump, one wavefront holding 64 W nodes
+//               (pointer jumping in LDS, no workgroup barrier): the delta
+//               rule's dense kernel (bf16, d = 128, node caps of up to 128)
+//               and the large-tree kernel of gated linear attention (bf16,
+//               d >= 32, caps of 65..256).
 // The depth of a node is its number of strict ancestors; where the routine
 // yields only the mask it is the mask's popcount minus one.
 #include <hip/hip_runtime.h>
@@ -32,7 +32,7 @@
 
 namespace tl {
 
-enum TopoKind { kTopoWaveN = 0, kTopoLds = 1, kTopoGdn = 2, kTopoWalk1 = 3 };
+enum TopoKind { kTopoWaveN = 0, kTopoLds = 1, kTopoGdn = 2, kTopoJump1 = 3 };
 
 template <int W>
 __device__ inline void store_topology(const TopoArgs& a, const Request& rq, int node, int dep,
@@ -55,7 +55,7 @@ __global__ __launch_bounds__(kThreads) void topology_kernel(TopoArgs a) {
   if (!load_request(a.node_offsets, blockIdx.x, a.max_nodes, a.dev_err, rq)) return;
   const int T = rq.T;
   if (T == 0) return;
-  if constexpr (KIND == kTopoWalk1) {
+  if constexpr (KIND == kTopoJump1) {
     if (tid >= 64) return;   // one wavefront; the others take no part
     int par[W];
     float x[W], cl[W];
@@ -65,7 +65,7 @@ __global__ __launch_bounds__(kThreads) void topology_kernel(TopoArgs a) {
       par[e] = a.parent[rq.off + min(tid + 64 * e, T - 1)];
       x[e] = 0.f;
     }
-    if (!wave_topology_walk<W, W>(par, x, T, s_jmp, s_acc, s_msk, cl, msk)) {
+    if (!wave_topology_jump<W, W>(par, x, T, s_jmp, s_acc, s_msk, cl, msk)) {
       if (tid == 0) report(a.dev_err, TL_EBADTREE);
       return;
     }
@@ -134,7 +134,9 @@ tl_status launch_topology(const tl_problem& p, const TopoArgs& a, hipStream_t st
   const int W = tm > 128 ? 4 : (tm > 64 ? 2 : 1);
   const bool mfma = p.in_dtype == TL_BF16 && p.d_k >= 32;
   if (mfma && p.mode == TL_MODE_GDN && p.d_k == 128 && tm <= 128)
-    return W == 1 ? launch_topo<kTopoWalk1, 1>(a, stream) : launch_topo<kTopoWalk1, 2>(a, stream);
+    return W == 1 ? launch_topo<kTopoJump1, 1>(a, stream) : launch_topo<kTopoJump1, 2>(a, stream);
+  if (mfma && p.mode == TL_MODE_GLA && tm > 64)
+    return W == 2 ? launch_topo<kTopoJump1, 2>(a, stream) : launch_topo<kTopoJump1, 4>(a, stream);
   if (mfma && p.mode == TL_MODE_GLA && tm <= 64)
     return (p.num_v_heads / p.num_qk_heads) % 2 == 0 ? launch_topo<kTopoWaveN, 1, 2>(a, stream)
                                                      : launch_topo<kTopoWaveN, 1, 1>(a, stream);

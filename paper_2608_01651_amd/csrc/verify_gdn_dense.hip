@@ -16,7 +16,7 @@
 // The node-by-node coupling sits in A = (I + G)^{-1}, a T x T matrix that does
 // not depend on the value channels.  So one workgroup of 8 wave64s per
 // (request, v-head) runs three phases separated by two barriers, after a
-// prologue in which wave 0 forms the topology alone (wave_topology_walk, no
+// prologue in which wave 0 forms the topology alone (wave_topology_jump, no
 // workgroup barrier) while waves 1..7 issue the K, Q and V copies:
 //  1. every wave forms its share of the 16 x 16 blocks (I, J <= I) of C and G
 //     (K_J Q_I^T and K_J K_I^T on MFMA, masked by the M+ rows, decayed) into
@@ -28,13 +28,15 @@
 //  2. wave J forms column block J of A: for I = J, J + 1, ...,
 //       X_I = (I + G_II)^{-1} (delta_IJ - sum_{J <= K < I} G_IK X_K),
 //     all on MFMA: X_K come out of the products as the B operands of the
-//     next ones.  Columns are independent, so the waves need no barrier
-//     between them.  A goes to LDS over the dead Q and K rows;
-//  3. every wave forms U = A R and O = q_scale (P B0 + C U) for its value
-//     channels: products of LDS operands (A, C) with register operands (R,
-//     U), no LDS round trip for the value side.
-// Blocks of C, G and A whose tile pair holds no ancestor relation are zero
-// and are neither formed nor read.  The matrices are fp32, split into bf16
+//     next ones, and so does column block J of C A, (C A)_IJ =
+//     sum_{J <= K <= I} C_IK X_K.  Columns are independent, so the waves
+//     need no barrier between them.  C A goes to LDS over the dead Q and K
+//     rows (A itself is never stored);
+//  3. every wave forms O = q_scale P B0 + (C A) R for its value channels
+//     (C U = C (A R)): products of an LDS operand (C A) with the register
+//     fragments of R, no LDS round trip for the value side.
+// Blocks of C, G, A and C A whose tile pair holds no ancestor relation are
+// zero and are neither formed nor read.  The matrices are fp32, split into bf16
 // hi + lo for the MFMA, with fp32 accumulation.
 #include <hip/hip_runtime.h>
 
@@ -102,7 +104,7 @@ __host__ __device__ inline DenseLayout dense_layout(int tm, int W) {
   L.tmask = o; o += align16(nb * W * 8);             // OR of M+ rows per node tile
   L.tin = o;   o += align16(nb * 4);                 // in-tile strict ancestors per tile
   L.gin = o;   o += nb * kTile * kTile * 4;          // in-tile blocks of G, row-major fp32
-  L.kq = o;                                          // K and Q rows | the blocks of A
+  L.kq = o;                                          // K and Q rows | the blocks of C A
   {
     const int rows = 2 * tm * 128 * 2, ablk = pair_row(nb) * 2048;
     o += rows > ablk ? rows : ablk;
@@ -167,7 +169,7 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   float* s_gin = reinterpret_cast<float*>(tl_lds + L.gin);
   __bf16* s_k = reinterpret_cast<__bf16*>(tl_lds + L.kq);
   __bf16* s_q = s_k + tm * D;
-  unsigned char* s_a = tl_lds + L.kq;      // blocks of A, over the dead K and Q rows
+  unsigned char* s_a = tl_lds + L.kq;      // blocks of C A, over the dead K and Q rows
   unsigned char* s_c = tl_lds + L.cst;
   __bf16* s_v = reinterpret_cast<__bf16*>(s_c);   // staged V rows, until the blocks of C are formed
   unsigned char* s_g = tl_lds + L.gst;
@@ -196,7 +198,12 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
       gx[e] = a.g[(size_t)i * a.Hv + h];
       bx[e] = a.beta[(size_t)i * a.Hv + h];
     }
-  } else {
+  }
+  // the parents and gates enter this CU's memory queue ahead of the bulk
+  // copies (a barrier without a memory wait: wave 0's loads are issued, not
+  // complete)
+  __builtin_amdgcn_s_barrier();
+  if (wave > 0) {   // uniform
     constexpr int CT = kDenseThreads - 64;
     for (int base = (wave - 1) * 64; base < T * CPRK; base += CT) {
       const int p = base + lane;
@@ -238,7 +245,7 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
     uint64_t* s_msk = reinterpret_cast<uint64_t*>(s_acc + 64 * NE);
     float cl[NE];
     uint64_t msk[NE][W];
-    const bool ok = wave_topology_walk<W, NE>(par, gx, T, s_jmp, s_acc, s_msk, cl, msk);
+    const bool ok = wave_topology_jump<W, NE>(par, gx, T, s_jmp, s_acc, s_msk, cl, msk);
     if (lane == 0) {
       *s_flag = ok ? 0 : 1;
       if (!ok) report(a.dev_err, TL_EBADTREE);
@@ -517,9 +524,16 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   // (node of tile J): per lane exactly the B-operand elements of a product
   // whose K index is i, so X_K feeds the later sums and Y feeds the in-tile
   // inverse without any transposition.  The sums run over pairs of node
-  // tiles (16x16x32, the stored -G as A operands); A_IJ goes to LDS in
-  // A-operand layout for phase 3.  Every block (I, J <= I) of A is written,
-  // zero where no ancestor relation.
+  // tiles (16x16x32, the stored -G as A operands).  With X_I the wave also
+  // forms block (I, J) of C A = sum_{J <= K <= I} C_IK X_K (the stored C as A
+  // operands), which goes to LDS in A-operand layout for phase 3, over the
+  // dead K and Q rows: O = C U = (C A) R.  Every block (I, J <= I) of C A is
+  // written, zero where no ancestor relation (an entry (i, j) of C A needs
+  // j in Anc(k) u {k} and k in Anc(i) u {i} for some k).
+  // pair P of row I of C (tiles 2 P, 2 P + 1) holds a nonzero block
+  auto pair_live = [&](int I, int P) __attribute__((always_inline)) {
+    return live(I, 2 * P) || (2 * P + 1 <= I && live(I, 2 * P + 1));
+  };
   if (wave < nt) {   // uniform
     const int J = wave;
     bf16x8 xph[NTM / 2], xpl[NTM / 2];   // X_K as B operands, tiles paired (zero below J)
@@ -528,7 +542,7 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
       xph[P] = bf16x8{};
       xpl[P] = bf16x8{};
     }
-    // X_I (row 4 lg + r, column lr) -> A_IJ in A-operand layout: lane
+    // block (row 4 lg + r, column lr) -> A-operand layout: lane
     // (4 lg + r) + 16 (lr / 4), element lr % 4 of half `half`
     auto store_a = [&](int pa, int half, const f32x4& x) __attribute__((always_inline)) {
       bf16x4 hi, lo;
@@ -546,7 +560,7 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
       if (I < J || I >= nt) return;   // uniform
       const int pa = pair_row(I) + J / 2;
       if (I == J && (I & 1) == 0) zero_half(s_a, pa, 1);   // (I, I + 1): never a block
-      if (!live(I, J)) {              // A_IJ = 0 (and X_I stays zero)
+      if (!live(I, J)) {              // A_IJ = 0, (C A)_IJ = 0 (and X_I stays zero)
         zero_half(s_a, pa, J & 1);
         return;
       }
@@ -573,40 +587,29 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
       f32x4 x2 = mfma16k(al, yh, f32x4{0.f, 0.f, 0.f, 0.f});
       x = mfma16k(ah, yl, x);
       x += x2;
-      store_a(pa, J & 1, x);   // A_IJ for phase 3
-      if (I + 1 < nt) set_half(xph[I / 2], xpl[I / 2], I & 1, x);
+      set_half(xph[I / 2], xpl[I / 2], I & 1, x);
+      // (C A)_IJ = sum_{J <= K <= I} C_IK X_K over tile pairs (the half
+      // K = I + 1 of the last pair is zero in both)
+      f32x4 ca = f32x4{0.f, 0.f, 0.f, 0.f}, ca2 = ca;
+#pragma unroll
+      for (int P = 0; 2 * P <= I; ++P) {
+        if (2 * P + 1 < J || !pair_live(I, P)) continue;   // uniform: X or C is zero
+        bf16x8 ch, cl;
+        get_pair(s_c, pair_row(I) + P, ch, cl);
+        ca = mfma16(ch, xph[P], ca);
+        ca2 = mfma16(ch, xpl[P], ca2);
+        ca = mfma16(cl, xph[P], ca);
+      }
+      store_a(pa, J & 1, ca + ca2);
     };
     static_for<NTM>(step_tile);
   }
-  lds_barrier();   // A is in LDS
+  lds_barrier();   // C A is in LDS
   TL_TRACE_POINT(a, 5);
 
-  // ---- 3. U = A R, then O = q_scale (P B0 + C U), for this wave's channels:
-  // 16x16x32 products over pairs of node tiles, both operands read whole
-  bf16x8 uph[NTM / 2], upl[NTM / 2];
-#pragma unroll
-  for (int P = 0; P < NTM / 2; ++P) {
-    uph[P] = bf16x8{};
-    upl[P] = bf16x8{};
-  }
-  auto pair_live = [&](int I, int P) __attribute__((always_inline)) {
-    return live(I, 2 * P) || (2 * P + 1 <= I && live(I, 2 * P + 1));
-  };
-#pragma unroll
-  for (int I = 0; I < NTM; ++I) {
-    if (I >= nt) break;   // uniform
-    f32x4 u = f32x4{0.f, 0.f, 0.f, 0.f}, u2 = u;
-#pragma unroll
-    for (int P = 0; 2 * P <= I; ++P) {
-      if (!pair_live(I, P)) continue;   // uniform
-      bf16x8 ah, al;
-      get_pair(s_a, pair_row(I) + P, ah, al);
-      u = mfma16(ah, rph[P], u);
-      u2 = mfma16(ah, rpl[P], u2);
-      u = mfma16(al, rph[P], u);
-    }
-    set_half(uph[I / 2], upl[I / 2], I & 1, u + u2);
-  }
+  // ---- 3. O = q_scale P B0 + (C A) R for this wave's channels: 16x16x32
+  // products over pairs of node tiles, C A read whole from LDS, R the
+  // register fragments
   float* obase = a.out + (size_t)(off + 4 * lg) * v_row + (size_t)h * D + kTile * wave + lr;
 #pragma unroll
   for (int I = 0; I < NTM; ++I) {
@@ -615,11 +618,11 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
 #pragma unroll
     for (int P = 0; 2 * P <= I; ++P) {
       if (!pair_live(I, P)) continue;   // uniform
-      bf16x8 ch, cl;
-      get_pair(s_c, pair_row(I) + P, ch, cl);
-      o = mfma16(ch, uph[P], o);
-      o2 = mfma16(ch, upl[P], o2);
-      o = mfma16(cl, uph[P], o);
+      bf16x8 ah, al;
+      get_pair(s_a, pair_row(I) + P, ah, al);
+      o = mfma16(ah, rph[P], o);
+      o2 = mfma16(ah, rpl[P], o2);
+      o = mfma16(al, rph[P], o);
     }
     const f32x4 cli = *reinterpret_cast<const f32x4*>(s_cl + kTile * I + 4 * lg);
     float* orow = obase + (size_t)(kTile * I) * v_row;

@@ -16,15 +16,16 @@
 // register is first read while a store is pending; a walk that read
 // prefetched rows waited for the previous tile's stores at every tile.)
 //
-//  prologue  batch 1: parents and gates (thread = node), the wave's state
-//            rows (registers), and, by direct global -> LDS copies, the V rows
-//            (into the K region; rows past T repeat row T - 1) and the Q rows.
-//            Each value wave then reads its V^T operand fragments of every
-//            32-node chunk out of the staged rows with LDS transpose reads
-//            (ds_read_b64_tr_b16; 32 VGPRs at 256 nodes), entries of nodes
-//            >= T set to zero.  Batch 2 copies the K rows over the staged V
-//            rows while the topology is built (M+ rows, cl, per-tile OR of the
-//            M+ rows; LDS pointer jumping, whose barriers wait for LDS only).
+//  prologue  batch 1: wave 0 loads the parents and gates and forms the
+//            topology alone (M+ rows, cl, per-tile OR of the M+ rows; pointer
+//            jumping in LDS with no workgroup barrier) while the other
+//            waves copy, by direct global -> LDS copies, the V rows (into the
+//            K region; rows past T repeat row T - 1) and the Q rows; every
+//            value wave loads its state rows (registers).  Each value wave
+//            then reads its V^T operand fragments of every 32-node chunk out
+//            of the staged rows with LDS transpose reads (ds_read_b64_tr_b16;
+//            32 VGPRs at 256 nodes), entries of nodes >= T set to zero.
+//            Batch 2 copies the K rows over the staged V rows.
 //  tile I    (a) coefficients: the ancestor columns of a tile are cut into
 //            chunks of 32 nodes (tiles 2c, 2c + 1) and dealt out to the waves
 //            by half chunk (one 16-node tile J).  A half chunk is one K_J
@@ -53,7 +54,7 @@ __host__ __device__ constexpr int gla_large_waves(int D) { return D / kTile > kW
 __host__ __device__ constexpr int gla_large_rows(int tm) { return (tm + 31) & ~31; }
 
 struct GlaLargeLayout {
-  int cl, mask, tmask, kst, qst, frag, fragsz, frag2, total;
+  int flag, cl, mask, tmask, kst, qst, frag, fragsz, frag2, total;
 };
 
 // Where the chunk operands of odd node tiles go.  kBufTwo: a second buffer
@@ -69,6 +70,7 @@ enum GlaLargeBuf { kBufTwo = 1, kBufK = 2 };
 __host__ __device__ inline GlaLargeLayout gla_large_layout(int D, int tm, int W, int buf) {
   GlaLargeLayout L;
   int o = 0;
+  L.flag = o;  o += 16;                                  // the tree is malformed
   L.cl = o;    o += align16(tm * 4);                     // cumulative log2-decay (0 past T)
   L.mask = o;  o += tm * W * 8;                          // M+ rows (0 past T)
   L.tmask = o; o += align16((tm / kTile) * W * 8);       // OR of the M+ rows per node tile
@@ -76,7 +78,7 @@ __host__ __device__ inline GlaLargeLayout gla_large_layout(int D, int tm, int W,
   L.qst = o;   o += tm * D * 2;                          // Q rows, swizzled bf16
   L.frag = o;                                            // chunk operands | topology scratch
   L.fragsz = ((tm + 31) / 32) * 2 * 1024;                // chunks of tiles 0..I: C hi, C lo
-  const int topo = kThreads * (4 + 4 + 4) + kThreads * W * 8;
+  const int topo = 64 * W * (4 + 4) + 64 * W * W * 8;   // wave_topology_jump scratch
   const int fr = (buf == kBufTwo ? 2 : 1) * L.fragsz;
   o += align16(fr > topo ? fr : topo);
   L.frag2 = buf == kBufTwo ? L.frag + L.fragsz : (buf == kBufK ? L.kst : L.frag);
@@ -99,7 +101,7 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_wave
   constexpr int CPRK = D / 8;              // 16-byte chunks per row
   constexpr int NCH = 2 * W;               // 32-node chunks of the largest tree
   constexpr float kLog2e = 1.4426950408889634f;
-  static_assert(NT >= 64 * W, "one thread per node in the topology");
+  constexpr int NE = W;                    // nodes per lane of wave 0 (node cap <= 64 W)
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63, lr = lane & 15, lg = lane >> 4;
@@ -138,26 +140,40 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_wave
   const __bf16* Kb = reinterpret_cast<const __bf16*>(a.k) + (size_t)off * qk_row + (size_t)hq * D;
   const __bf16* Vb = reinterpret_cast<const __bf16*>(a.v) + (size_t)off * v_row + (size_t)h * D;
 
-  // ---- prologue, batch 1: parents and gates, the V and Q rows into LDS,
-  // and the wave's state rows.  Copy position p = base + lane holds 16-byte chunk
-  // swz(r, p % CPRK) of row r = p / CPRK.
+  // ---- prologue, batch 1: wave 0 loads the parents and gates and its
+  // state rows, and forms the topology alone (wave_topology_jump, no
+  // workgroup barrier) while waves 1.. copy the V and Q rows into LDS and
+  // load their state rows.  Copy position p = base + lane holds 16-byte
+  // chunk swz(r, p % CPRK) of row r = p / CPRK.  The copies are inline
+  // assembly, which the compiler does not count, so wave 0, whose waits the
+  // compiler places, issues none.
   TL_TRACE_POINT(a, 1);
-  int par = -1;
-  float gx = 0.f;
-  if (tid < T) {
-    par = a.parent[off + tid];
-    gx = a.g[(size_t)(off + tid) * a.Hv + h];
+  int par[NE];
+  float gx[NE];
+  if (wave == 0) {   // uniform
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {   // unconditional loads, clamped to the tree
+      const int i = off + min(lane + 64 * e, T - 1);
+      par[e] = a.parent[i];
+      gx[e] = a.g[(size_t)i * a.Hv + h];
+    }
   }
+  // the parents and gates enter this CU's memory queue ahead of the bulk
+  // copies (a barrier without a memory wait: wave 0's loads are issued, not
+  // complete)
+  __builtin_amdgcn_s_barrier();
   const int TP = (T + 31) & ~31;   // V rows of every chunk the tree reads
-  for (int base = wave * 64; base < TP * CPRK; base += NT) {   // uniform; TP * CPRK is a multiple of 64
-    const int p = base + lane, r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
-    copy16_to_lds_async(Vb + (size_t)min(r, T - 1) * v_row + c * 8, s_k + (size_t)base * 8);
-  }
-  for (int base = wave * 64; base < T * CPRK; base += NT) {   // uniform
-    const int p = base + lane;
-    if (p < T * CPRK) {
-      const int r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
-      copy16_to_lds_async(Qb + (size_t)r * qk_row + c * 8, s_q + (size_t)base * 8);
+  if (wave > 0) {   // uniform
+    for (int base = (wave - 1) * 64; base < TP * CPRK; base += NT - 64) {   // TP * CPRK is a multiple of 64
+      const int p = base + lane, r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
+      copy16_to_lds_async(Vb + (size_t)min(r, T - 1) * v_row + c * 8, s_k + (size_t)base * 8);
+    }
+    for (int base = (wave - 1) * 64; base < T * CPRK; base += NT - 64) {
+      const int p = base + lane;
+      if (p < T * CPRK) {
+        const int r = p / CPRK, c = swz<CPRK>(r, p % CPRK);
+        copy16_to_lds_async(Qb + (size_t)r * qk_row + c * 8, s_q + (size_t)base * 8);
+      }
     }
   }
   // the wave's state rows last: the batch's wait leaves them in flight, and
@@ -171,13 +187,51 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_wave
       sraw[ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 16 + 4 * lg));
     }
   }
-  for (int x = tid; x < (tm / kTile) * W; x += NT) s_tmask[x] = 0;
+  // ---- topology by wave 0: M+ rows, cl, per-tile OR of the M+ rows (rows
+  // past T: zero masks and decays)
+  int* s_flag = reinterpret_cast<int*>(tl_lds + L.flag);
+  if (wave == 0) {   // uniform
+    for (int x = lane; x < (tm / kTile) * W; x += 64) s_tmask[x] = 0;
+    int* s_jmp = reinterpret_cast<int*>(s_frag);
+    float* s_acc = reinterpret_cast<float*>(s_jmp + 64 * NE);
+    uint64_t* s_msk = reinterpret_cast<uint64_t*>(s_acc + 64 * NE);
+    float cl[NE];
+    uint64_t msk[NE][W];
+    const bool ok = wave_topology_jump<W, NE>(par, gx, T, s_jmp, s_acc, s_msk, cl, msk);
+    if (lane == 0) {
+      *s_flag = ok ? 0 : 1;
+      if (!ok) report(a.dev_err, TL_EBADTREE);
+    }
+    if (ok) {   // uniform
+#pragma unroll
+      for (int e = 0; e < NE; ++e) {
+        const int i = lane + 64 * e;
+        if (i < tm) {
+          s_cl[i] = i < T ? cl[e] * kLog2e : 0.f;
+#pragma unroll
+          for (int w = 0; w < W; ++w) s_mask[i * W + w] = i < T ? msk[e][w] : 0ull;
+          if (i < T) {
+            const int I = i / kTile;
+#pragma unroll
+            for (int w = 0; w < W; ++w)
+              if (msk[e][w]) atomicOr(reinterpret_cast<unsigned long long*>(&s_tmask[I * W + w]),
+                                      (unsigned long long)msk[e][w]);
+          }
+        }
+      }
+    }
+  }
+  TL_TRACE_POINT(a, 13);
   // batch 1 but the state rows has landed (loads complete in issue order; a
-  // wait the compiler sees, so it knows the parents and gates are in)
+  // wait the compiler sees)
   if (vw) wait_vmem_below<2 * KS>();
   else wait_vmem_below<0>();
-  lds_barrier();          // staged V rows, Q rows and zeroed tile masks are visible
+  lds_barrier();          // staged V rows, Q rows and the topology are visible
   TL_TRACE_POINT(a, 2);
+  if (*s_flag) {   // uniform: a malformed tree (reported by wave 0)
+    wait_vmem();   // the state rows land before the block retires
+    return;
+  }
 
   // the wave's V^T operand fragments of every chunk: lane (lg, lr) names row
   // 4 lg + lr / 4 of a 16-node half chunk and columns 16 w + 4 (lr % 4) .. + 3,
@@ -213,7 +267,7 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_wave
   TL_TRACE_POINT(a, 11);
   lds_barrier();   // every wave has read the staged V rows
 
-  // ---- batch 2: K rows over the staged V rows, while the topology is built
+  // ---- batch 2: K rows over the staged V rows
   for (int base = wave * 64; base < T * CPRK; base += NT) {   // uniform
     const int p = base + lane;
     if (p < T * CPRK) {
@@ -222,34 +276,6 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_wave
     }
   }
   TL_TRACE_POINT(a, 3);
-  {
-    int* s_jmp = reinterpret_cast<int*>(s_frag);
-    float* s_acc = reinterpret_cast<float*>(s_jmp + kThreads);
-    int* s_cnt = reinterpret_cast<int*>(s_acc + kThreads);
-    uint64_t* s_msk = reinterpret_cast<uint64_t*>(s_cnt + kThreads);
-    int dep = 0;
-    float cl = 0.f;
-    uint64_t msk[W];
-    const bool ok = build_topology<W, true>(par, T, gx, s_jmp, s_acc, s_cnt, s_msk, dep, cl, msk);
-    if (!ok) {
-      if (tid == 0) report(a.dev_err, TL_EBADTREE);
-      wait_vmem();   // let the in-flight LDS copies land before the block retires
-      return;
-    }
-    TL_TRACE_POINT(a, 13);
-    if (tid < tm) {   // rows past T: zero masks and decays
-      s_cl[tid] = tid < T ? cl * kLog2e : 0.f;
-#pragma unroll
-      for (int w = 0; w < W; ++w) s_mask[tid * W + w] = tid < T ? msk[w] : 0ull;
-      if (tid < T) {
-        const int I = tid / kTile;
-#pragma unroll
-        for (int w = 0; w < W; ++w)
-          if (msk[w]) atomicOr(reinterpret_cast<unsigned long long*>(&s_tmask[I * W + w]),
-                               (unsigned long long)msk[w]);
-      }
-    }
-  }
   // the wave's state rows, split into bf16 hi + lo MFMA A operands
   bf16x8 shi[KS], slo[KS];
   if (vw) {
@@ -258,7 +284,7 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_wave
   }
   TL_TRACE_POINT(a, 14);
   wait_vmem();     // batch 2 (the K rows) has landed
-  lds_barrier();   // K rows, M+ rows, tile masks and decays are visible; the topology scratch is dead
+  lds_barrier();   // K rows are visible; the topology scratch is dead
   TL_TRACE_POINT(a, 4);
 
   // operand fragment of row R + lr (R a multiple of 16), K chunk ks, of a
