@@ -28,13 +28,15 @@
 
 namespace tl {
 
-// f(std::integral_constant<int, J>{}) for J = 0 .. N-1, in order.
+// f(std::integral_constant<int, J>{}) for J = 0 .. N-1, in order.  Always
+// inlined: the bodies are whole kernel phases, and an outlined call would
+// give them a stack frame and the calling convention's register budget.
 template <class F, int... J>
-__device__ inline void static_for_seq(F& f, std::integer_sequence<int, J...>) {
+__device__ __attribute__((always_inline)) inline void static_for_seq(F& f, std::integer_sequence<int, J...>) {
   (f(std::integral_constant<int, J>{}), ...);
 }
 template <int N, class F>
-__device__ inline void static_for(F& f) {
+__device__ __attribute__((always_inline)) inline void static_for(F& f) {
   static_for_seq(f, std::make_integer_sequence<int, N>{});
 }
 

@@ -542,19 +542,6 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
       xph[P] = bf16x8{};
       xpl[P] = bf16x8{};
     }
-    // block (row 4 lg + r, column lr) -> A-operand layout: lane
-    // (4 lg + r) + 16 (lr / 4), element lr % 4 of half `half`
-    auto store_a = [&](int pa, int half, const f32x4& x) __attribute__((always_inline)) {
-      bf16x4 hi, lo;
-      split4_bf16(x, hi, lo);
-      unsigned char* q = s_a + pa * 2048 + half * 8 + (lr & 3) * 2;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int t = 4 * lg + r + 16 * (lr >> 2);
-        *reinterpret_cast<__bf16*>(q + t * 16) = hi[r];
-        *reinterpret_cast<__bf16*>(q + 1024 + t * 16) = lo[r];
-      }
-    };
     auto step_tile = [&](auto Ic) __attribute__((always_inline)) {
       constexpr int I = decltype(Ic)::value;
       if (I < J || I >= nt) return;   // uniform
@@ -589,18 +576,22 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
       x += x2;
       set_half(xph[I / 2], xpl[I / 2], I & 1, x);
       // (C A)_IJ = sum_{J <= K <= I} C_IK X_K over tile pairs (the half
-      // K = I + 1 of the last pair is zero in both)
+      // K = I + 1 of the last pair is zero in both), formed transposed: with
+      // the X fragments as A operands and the stored C as B operands, the
+      // product comes back with column i and rows j, so a lane holds row i
+      // of (C A)_IJ at the K positions of its lane group, which is its part
+      // of the A operand of phase 3 as it stands (no transposition)
       f32x4 ca = f32x4{0.f, 0.f, 0.f, 0.f}, ca2 = ca;
 #pragma unroll
       for (int P = 0; 2 * P <= I; ++P) {
         if (2 * P + 1 < J || !pair_live(I, P)) continue;   // uniform: X or C is zero
         bf16x8 ch, cl;
         get_pair(s_c, pair_row(I) + P, ch, cl);
-        ca = mfma16(ch, xph[P], ca);
-        ca2 = mfma16(ch, xpl[P], ca2);
-        ca = mfma16(cl, xph[P], ca);
+        ca = mfma16(xph[P], ch, ca);
+        ca2 = mfma16(xpl[P], ch, ca2);
+        ca = mfma16(xph[P], cl, ca);
       }
-      store_a(pa, J & 1, ca + ca2);
+      put_half(s_a, pa, J & 1, ca + ca2);
     };
     static_for<NTM>(step_tile);
   }
