@@ -534,8 +534,8 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   auto pair_live = [&](int I, int P) __attribute__((always_inline)) {
     return live(I, 2 * P) || (2 * P + 1 <= I && live(I, 2 * P + 1));
   };
-  if (wave < nt) {   // uniform
-    const int J = wave;
+  // Column block J, generic form: any tree, dead blocks skipped.
+  auto column_any = [&](int J) __attribute__((always_inline)) {
     bf16x8 xph[NTM / 2], xpl[NTM / 2];   // X_K as B operands, tiles paired (zero below J)
 #pragma unroll
     for (int P = 0; P < NTM / 2; ++P) {
@@ -594,6 +594,76 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
       put_half(s_a, pa, J & 1, ca + ca2);
     };
     static_for<NTM>(step_tile);
+  };
+  // Column block J of a full tree (node tiles 0..NTM - 1), J a compile-time
+  // constant: no branch at all, so the compiler can issue a step's LDS reads
+  // (G, the in-tile inverse, C) during the products of the step before.
+  // Dead blocks are formed too: every term of their products pairs a zero
+  // coefficient with a zero X entry or the other way round, so they come
+  // out exactly zero for finite inputs (a non-finite input of the request
+  // may spread through them, within the bounds the delta rule documents).
+  auto column_full = [&](auto Jc) __attribute__((always_inline)) {
+    constexpr int J = decltype(Jc)::value;
+    bf16x8 xph[NTM / 2], xpl[NTM / 2];
+#pragma unroll
+    for (int P = 0; P < NTM / 2; ++P) {
+      xph[P] = bf16x8{};
+      xpl[P] = bf16x8{};
+    }
+    auto step_tile = [&](auto Ic) __attribute__((always_inline)) {
+      constexpr int I = decltype(Ic)::value;
+      if constexpr (I >= J) {
+        constexpr int pa = pair_row(I) + J / 2;
+        if constexpr (I == J && (I & 1) == 0) zero_half(s_a, pa, 1);   // (I, I + 1): never a block
+        const bf16x4 ah = *reinterpret_cast<const bf16x4*>(s_ainv + I * 1024 + lane * 8);
+        const bf16x4 al = *reinterpret_cast<const bf16x4*>(s_ainv + I * 1024 + 512 + lane * 8);
+        f32x4 y, y2 = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[r] = (I == J && 4 * lg + r == lr) ? 1.f : 0.f;
+#pragma unroll
+        for (int P = (J & ~1) / 2; 2 * P < I; ++P) {   // pairs below J / 2 hold zero X
+          bf16x8 gh, gl;
+          get_pair(s_g, gpair_row(I) + P, gh, gl);
+          y = mfma16(gh, xph[P], y);
+          y2 = mfma16(gl, xph[P], y2);
+          y = mfma16(gh, xpl[P], y);
+        }
+        y += y2;
+        bf16x4 yh, yl;
+        split4_bf16(y, yh, yl);
+        f32x4 x = mfma16k(ah, yh, f32x4{0.f, 0.f, 0.f, 0.f});
+        f32x4 x2 = mfma16k(al, yh, f32x4{0.f, 0.f, 0.f, 0.f});
+        x = mfma16k(ah, yl, x);
+        x += x2;
+        set_half(xph[I / 2], xpl[I / 2], I & 1, x);
+        f32x4 ca = f32x4{0.f, 0.f, 0.f, 0.f}, ca2 = ca;
+#pragma unroll
+        for (int P = (J & ~1) / 2; 2 * P <= I; ++P) {
+          bf16x8 ch, cl;
+          get_pair(s_c, pair_row(I) + P, ch, cl);
+          ca = mfma16(xph[P], ch, ca);
+          ca2 = mfma16(xpl[P], ch, ca2);
+          ca = mfma16(xph[P], cl, ca);
+        }
+        put_half(s_a, pa, J & 1, ca + ca2);
+      }
+    };
+    static_for<NTM>(step_tile);
+  };
+  if (nt == NTM) {   // uniform
+    switch (wave) {   // uniform
+      case 0: column_full(std::integral_constant<int, 0>{}); break;
+      case 1: column_full(std::integral_constant<int, 1>{}); break;
+      case 2: column_full(std::integral_constant<int, 2>{}); break;
+      case 3: column_full(std::integral_constant<int, 3>{}); break;
+      case 4: column_full(std::integral_constant<int, 4>{}); break;
+      case 5: column_full(std::integral_constant<int, 5>{}); break;
+      case 6: column_full(std::integral_constant<int, 6>{}); break;
+      default: column_full(std::integral_constant<int, 7>{}); break;
+    }
+    static_assert(NTM == kDenseWaves, "one column block per wave");
+  } else if (wave < nt) {   // uniform
+    column_any(wave);
   }
   lds_barrier();   // C A is in LDS
   TL_TRACE_POINT(a, 5);

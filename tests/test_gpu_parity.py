@@ -122,8 +122,11 @@ def _forest(T, roots, rng):
     ("production", W.GLA, 128, 64, 16, 32),   # small-tree kernel, two v-heads per block
     ("production", W.GLA, 64, 48, 3, 3),      # small-tree kernel, one v-head per block
     ("gdn", W.GDN, 128, 256, 2, 4),           # the delta rule's wide-cap kernel
+    ("gdn", W.GDN, 128, 128, 2, 4),           # dense kernel: one-wave pointer jumping, 2 mask words
+    ("gdn", W.GDN, 128, 64, 2, 4),            # dense kernel: one-wave pointer jumping, 1 mask word
     ("gdn", W.GDN, 64, 128, 2, 4),            # tile walk, 2 mask words
-    ("large", W.GLA, 128, 200, 2, 4),         # tile walk, 4 mask words
+    ("large", W.GLA, 128, 200, 2, 4),         # large-tree kernel: one-wave pointer jumping, 4 words
+    ("large", W.GLA, 64, 100, 2, 4),          # large-tree kernel: one-wave pointer jumping, 2 words
     ("tiny", W.GLA, 16, 64, 1, 1),            # vector path (fp32 inputs)
 ])
 def test_topology_export_per_kernel(base, mode, d, max_nodes, hk, hv):
