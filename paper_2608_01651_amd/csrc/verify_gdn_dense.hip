@@ -427,14 +427,6 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
       else zero_half(s_g, gpair_row(I) + I / 2, 1);
     }
   };
-  // two blocks per step (block k goes to wave k % 8)
-  for (int k = wave; k < nblk; k += 2 * kDenseWaves) {   // uniform
-    const int k2 = k + kDenseWaves;
-    f32x4 cv[2], gv[2];
-    form2(k, min(k2, nblk - 1), cv, gv);
-    store(k, cv[0], gv[0]);
-    if (k2 < nblk) store(k2, cv[1], gv[1]);
-  }
   // ---- 1a'. the in-tile inverses (I + G_II)^{-1}, by the wave that formed
   // block (I, I) (block k = I (I + 3) / 2 goes to wave k % 8), from the
   // in-tile block it stored itself: forward substitution on the identity
@@ -442,10 +434,8 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   // 16-lane row holds x_s and broadcasts it by DPP row_newbcast).  Lane
   // (lr, lg) then holds row lr, columns 4 lg .. + 3 of the inverse: the A
   // operand of a 16x16x16 product.
-  auto make_ainv = [&](auto Ic) __attribute__((always_inline)) {
+  auto ainv_body = [&](auto Ic) __attribute__((always_inline)) {
     constexpr int I = decltype(Ic)::value;
-    constexpr int kdiag = I * (I + 3) / 2;
-    if (I >= nt || kdiag % kDenseWaves != wave) return;   // uniform
     const float* gi = s_gin + I * kTile * kTile + lr * kTile;
     const f32x4 g0 = *reinterpret_cast<const f32x4*>(gi), g1 = *reinterpret_cast<const f32x4*>(gi + 4),
                 g2 = *reinterpret_cast<const f32x4*>(gi + 8), g3 = *reinterpret_cast<const f32x4*>(gi + 12);
@@ -471,7 +461,58 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
     *reinterpret_cast<bf16x4*>(s_ainv + I * 1024 + lane * 8) = hi;
     *reinterpret_cast<bf16x4*>(s_ainv + I * 1024 + 512 + lane * 8) = lo;
   };
-  static_for<NTM>(make_ainv);
+  auto make_ainv = [&](auto Ic) __attribute__((always_inline)) {
+    constexpr int I = decltype(Ic)::value;
+    constexpr int kdiag = I * (I + 3) / 2;
+    if (I >= nt || kdiag % kDenseWaves != wave) return;   // uniform
+    ainv_body(Ic);
+  };
+  // 1a of a full tree (node tiles 0..NTM - 1) for wave w, a compile-time
+  // constant: blocks w, w + 8, ... and the inverses of the diagonal blocks
+  // among them, with no branch, so that the compiler can overlap the reads
+  // of one pair of blocks with the products of the one before
+  auto phase1a_full = [&](auto Wc) __attribute__((always_inline)) {
+    constexpr int w = decltype(Wc)::value;
+    constexpr int nb = tri(NTM);
+    auto pair_of = [&](auto Mc) __attribute__((always_inline)) {
+      constexpr int k = w + 2 * kDenseWaves * decltype(Mc)::value;
+      if constexpr (k < nb) {
+        constexpr int k2 = k + kDenseWaves < nb ? k + kDenseWaves : k;
+        f32x4 cv[2], gv[2];
+        form2(k, k2, cv, gv);
+        store(k, cv[0], gv[0]);
+        if constexpr (k2 != k) store(k2, cv[1], gv[1]);
+      }
+    };
+    static_for<(nb + 2 * kDenseWaves - 1) / (2 * kDenseWaves)>(pair_of);
+    auto inv = [&](auto Ic) __attribute__((always_inline)) {
+      constexpr int I = decltype(Ic)::value;
+      if constexpr ((I * (I + 3) / 2) % kDenseWaves == w) ainv_body(Ic);
+    };
+    static_for<NTM>(inv);
+  };
+  if (nt == NTM) {   // uniform
+    switch (wave) {   // uniform
+      case 0: phase1a_full(std::integral_constant<int, 0>{}); break;
+      case 1: phase1a_full(std::integral_constant<int, 1>{}); break;
+      case 2: phase1a_full(std::integral_constant<int, 2>{}); break;
+      case 3: phase1a_full(std::integral_constant<int, 3>{}); break;
+      case 4: phase1a_full(std::integral_constant<int, 4>{}); break;
+      case 5: phase1a_full(std::integral_constant<int, 5>{}); break;
+      case 6: phase1a_full(std::integral_constant<int, 6>{}); break;
+      default: phase1a_full(std::integral_constant<int, 7>{}); break;
+    }
+  } else {
+    // two blocks per step (block k goes to wave k % 8)
+    for (int k = wave; k < nblk; k += 2 * kDenseWaves) {   // uniform
+      const int k2 = k + kDenseWaves;
+      f32x4 cv[2], gv[2];
+      form2(k, min(k2, nblk - 1), cv, gv);
+      store(k, cv[0], gv[0]);
+      if (k2 < nblk) store(k2, cv[1], gv[1]);
+    }
+    static_for<NTM>(make_ainv);
+  }
   TL_TRACE_POINT(a, 8);
 
   // ---- 1b. B0 = Q S^T and SK = K S^T for this wave's channels, all node tiles
@@ -488,32 +529,38 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   for (int ks = 0; ks < KS; ++ks) split8_bf16(sraw[ks][0], sraw[ks][1], shi[ks], slo[ks]);
 
   TL_TRACE_POINT(a, 9);
+  auto tile1b = [&](auto Ic) __attribute__((always_inline)) {
+    constexpr int I = decltype(Ic)::value;
+    f32x4 bb = f32x4{0.f, 0.f, 0.f, 0.f}, sk = bb;
 #pragma unroll
-  for (int I = 0; I < NTM; ++I) {
-    b0[I] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (I < nt) {   // uniform
-      f32x4 sk = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 qf = frag(s_q, kTile * I, ks), kf = frag(s_k, kTile * I, ks);
-        b0[I] = mfma16(qf, shi[ks], b0[I]);
-        sk = mfma16(kf, shi[ks], sk);
-        b0[I] = mfma16(qf, slo[ks], b0[I]);
-        sk = mfma16(kf, slo[ks], sk);
-      }
-      // R_j = beta_j (v_j - P_j (S k_j)); zero past the tree (those columns of
-      // A meet only zero coefficients, and must stay finite)
-      const f32x4 clj = *reinterpret_cast<const f32x4*>(s_cl + kTile * I + 4 * lg);
-      const f32x4 bj = *reinterpret_cast<const f32x4*>(s_beta + kTile * I + 4 * lg);
-      f32x4 rv;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const bool jv = kTile * I + 4 * lg + r < T;
-        rv[r] = jv ? bj[r] * ((float)vv[I][r] - __builtin_amdgcn_exp2f(clj[r]) * sk[r]) : 0.f;
-      }
-      set_half(rph[I / 2], rpl[I / 2], I & 1, rv);
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 qf = frag(s_q, kTile * I, ks), kf = frag(s_k, kTile * I, ks);
+      bb = mfma16(qf, shi[ks], bb);
+      sk = mfma16(kf, shi[ks], sk);
+      bb = mfma16(qf, slo[ks], bb);
+      sk = mfma16(kf, slo[ks], sk);
     }
-  }
+    b0[I] = bb;
+    // R_j = beta_j (v_j - P_j (S k_j)); zero past the tree (those columns of
+    // A meet only zero coefficients, and must stay finite)
+    const f32x4 clj = *reinterpret_cast<const f32x4*>(s_cl + kTile * I + 4 * lg);
+    const f32x4 bj = *reinterpret_cast<const f32x4*>(s_beta + kTile * I + 4 * lg);
+    f32x4 rv;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const bool jv = kTile * I + 4 * lg + r < T;
+      rv[r] = jv ? bj[r] * ((float)vv[I][r] - __builtin_amdgcn_exp2f(clj[r]) * sk[r]) : 0.f;
+    }
+    set_half(rph[I / 2], rpl[I / 2], I & 1, rv);
+  };
+  auto tile1b_any = [&](auto Ic) __attribute__((always_inline)) {
+    if (decltype(Ic)::value < nt) tile1b(Ic);   // uniform
+    else b0[decltype(Ic)::value] = f32x4{0.f, 0.f, 0.f, 0.f};
+  };
+  // (a branch-free form for full trees measured slower: 1b's tiles are
+  // independent, and the compiler hoisted reads of later tiles at the cost
+  // of registers)
+  static_for<NTM>(tile1b_any);
   TL_TRACE_POINT(a, 10);
   lds_barrier();   // C, G and the in-tile inverses are in LDS; K and Q are dead
   TL_TRACE_POINT(a, 4);
@@ -672,13 +719,15 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   // products over pairs of node tiles, C A read whole from LDS, R the
   // register fragments
   float* obase = a.out + (size_t)(off + 4 * lg) * v_row + (size_t)h * D + kTile * wave + lr;
-#pragma unroll
-  for (int I = 0; I < NTM; ++I) {
-    if (I >= nt) break;   // uniform
+  // tile I of phase 3; ALL: every row of the tile is a node (no store test)
+  // and dead pairs are read as the zeros they hold (no branch)
+  auto tile3 = [&](auto Ic, auto ALLc) __attribute__((always_inline)) {
+    constexpr int I = decltype(Ic)::value;
+    constexpr bool ALL = decltype(ALLc)::value;
     f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f}, o2 = o;
 #pragma unroll
     for (int P = 0; 2 * P <= I; ++P) {
-      if (!pair_live(I, P)) continue;   // uniform
+      if (!ALL && !pair_live(I, P)) continue;   // uniform
       bf16x8 ah, al;
       get_pair(s_a, pair_row(I) + P, ah, al);
       o = mfma16(ah, rph[P], o);
@@ -690,9 +739,15 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const float v = a.q_scale * __builtin_amdgcn_exp2f(cli[r]) * b0[I][r] + (o[r] + o2[r]);
-      if (kTile * I + 4 * lg + r < T) __builtin_nontemporal_store(v, orow + (size_t)r * v_row);
+      if (ALL || kTile * I + 4 * lg + r < T) __builtin_nontemporal_store(v, orow + (size_t)r * v_row);
     }
-  }
+  };
+  auto tile3_all = [&](auto Ic) __attribute__((always_inline)) { tile3(Ic, std::true_type{}); };
+  auto tile3_any = [&](auto Ic) __attribute__((always_inline)) {
+    if (decltype(Ic)::value < nt) tile3(Ic, std::false_type{});   // uniform
+  };
+  if (T == kTile * NTM) static_for<NTM>(tile3_all);   // uniform
+  else static_for<NTM>(tile3_any);
   TL_TRACE_POINT(a, 15);
 #ifdef TL_TRACE
   if (a.trace && threadIdx.x == 0) a.trace[(size_t)blockIdx.x * 16 + 14] = (long long)__builtin_readcyclecounter();
