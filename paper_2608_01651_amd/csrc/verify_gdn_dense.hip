@@ -471,25 +471,79 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   // constant: blocks w, w + 8, ... and the inverses of the diagonal blocks
   // among them, with no branch, so that the compiler can overlap the reads
   // of one pair of blocks with the products of the one before
+  // Blocks (I, J0 .. J0 + NJ - 1) of one row, I, J0, NJ compile-time
+  // constants: the row's Q_I and K_I fragments are read once for all of them
+  // (K_J once per block), then their MFMA chains run side by side.
+  auto form_row = [&](auto Ic, auto J0c, auto NJc) __attribute__((always_inline)) {
+    constexpr int I = decltype(Ic)::value, J0 = decltype(J0c)::value, NJ = decltype(NJc)::value;
+    bf16x8 qi[KS], ki[KS], kj[NJ][KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      qi[ks] = frag(s_q, kTile * I, ks);
+      ki[ks] = frag(s_k, kTile * I, ks);
+#pragma unroll
+      for (int b = 0; b < NJ; ++b) kj[b][ks] = frag(s_k, kTile * (J0 + b), ks);
+    }
+    const int i = kTile * I + lr;
+    const bool iv = i < T;
+    const float cli = iv ? s_cl[i] : 0.f, bi = iv ? s_beta[min(i, tm - 1)] : 0.f;
+    uint64_t mw[W];
+#pragma unroll
+    for (int w = 0; w < W; ++w) mw[w] = iv ? s_mask[min(i, tm - 1) * W + w] : 0ull;
+    f32x4 qk[NJ], kk[NJ];
+#pragma unroll
+    for (int b = 0; b < NJ; ++b) qk[b] = kk[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int b = 0; b < NJ; ++b) {
+        qk[b] = mfma16(kj[b][ks], qi[ks], qk[b]);
+        kk[b] = mfma16(kj[b][ks], ki[ks], kk[b]);
+      }
+#pragma unroll
+    for (int b = 0; b < NJ; ++b) {
+      const int J = J0 + b;
+      const f32x4 clj = *reinterpret_cast<const f32x4*>(s_cl + kTile * J + 4 * lg);
+      const unsigned mb = (unsigned)(mw[J >> 2] >> ((J & 3) * kTile + 4 * lg)) & 0xFu;
+      f32x4 cv, gv;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool m = (mb >> r) & 1u;
+        const bool self = J == I && 4 * lg + r == lr;
+        const float dec = __builtin_amdgcn_exp2f(cli - clj[r]);
+        const float c = (dec * a.q_scale) * qk[b][r], g = (bi * dec) * kk[b][r];
+        cv[r] = m ? c : 0.f;
+        gv[r] = (m && !self) ? g : 0.f;
+      }
+      store(tri(I) + J, cv, gv);
+    }
+  };
+  // 1a of a full tree (node tiles 0..NTM - 1) for wave w, a compile-time
+  // constant, with no branch.  The rows are paired (I, NTM - 1 - I): 9
+  // blocks a pair, split over two waves so that each takes a contiguous run
+  // of one row's blocks (sharing that row's fragments), plus at most a run
+  // of the other row, and the diagonal blocks' inverses go with them:
+  //   w0: (7, 0..3) (0, 0)      w1: (7, 4..7)
+  //   w2: (6, 0..4)             w3: (6, 5..6) (1, 0..1)
+  //   w4: (5, 0..3) (2, 0)      w5: (5, 4..5) (2, 1..2)
+  //   w6: (4, 0..4)             w7: (3, 0..3)
   auto phase1a_full = [&](auto Wc) __attribute__((always_inline)) {
     constexpr int w = decltype(Wc)::value;
-    constexpr int nb = tri(NTM);
-    auto pair_of = [&](auto Mc) __attribute__((always_inline)) {
-      constexpr int k = w + 2 * kDenseWaves * decltype(Mc)::value;
-      if constexpr (k < nb) {
-        constexpr int k2 = k + kDenseWaves < nb ? k + kDenseWaves : k;
-        f32x4 cv[2], gv[2];
-        form2(k, k2, cv, gv);
-        store(k, cv[0], gv[0]);
-        if constexpr (k2 != k) store(k2, cv[1], gv[1]);
-      }
-    };
-    static_for<(nb + 2 * kDenseWaves - 1) / (2 * kDenseWaves)>(pair_of);
-    auto inv = [&](auto Ic) __attribute__((always_inline)) {
-      constexpr int I = decltype(Ic)::value;
-      if constexpr ((I * (I + 3) / 2) % kDenseWaves == w) ainv_body(Ic);
-    };
-    static_for<NTM>(inv);
+    static_assert(NTM == 8 && kDenseWaves == 8, "the row pairing is written for 8 tiles and 8 waves");
+    using std::integral_constant;
+    constexpr int p = w / 2, hi = NTM - 1 - p, lo = p;   // the row pair
+    // the split of the pair's 9 blocks: (run of row hi) + (run of row lo)
+    constexpr int hiJ0[8] = {0, 4, 0, 5, 0, 4, 0, 0};
+    constexpr int hiN[8] = {4, 4, 5, 2, 4, 2, 5, 0};
+    constexpr int loJ0[8] = {0, 0, 0, 0, 0, 1, 0, 0};
+    constexpr int loN[8] = {1, 0, 0, 2, 1, 2, 0, 4};
+    if constexpr (hiN[w] > 0) form_row(integral_constant<int, hi>{}, integral_constant<int, hiJ0[w]>{},
+                                       integral_constant<int, hiN[w]>{});
+    if constexpr (loN[w] > 0) form_row(integral_constant<int, lo>{}, integral_constant<int, loJ0[w]>{},
+                                       integral_constant<int, loN[w]>{});
+    // the inverses of the diagonal blocks this wave formed
+    if constexpr (hiN[w] > 0 && hiJ0[w] + hiN[w] - 1 == hi) ainv_body(integral_constant<int, hi>{});
+    if constexpr (loN[w] > 0 && loJ0[w] + loN[w] - 1 == lo) ainv_body(integral_constant<int, lo>{});
   };
   if (nt == NTM) {   // uniform
     switch (wave) {   // uniform
