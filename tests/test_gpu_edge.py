@@ -403,6 +403,31 @@ def test_tile_walk_delta_rule_single_buffer(d, max_nodes, sizes):
     assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
 
 
+def test_delta_rule_dense_kernel_tile_counts():
+    """The delta rule's dense kernel (d = 128, node cap 128) has branch-free
+    code for trees that fill all 8 node tiles (113..128 nodes) and, when
+    every row of the last tile is a node (128 nodes), for the readout too;
+    other trees take the generic code.  One batch with trees of 128, 127,
+    120 and 113 nodes (full tiles, the last one ragged), 112 and 40 (fewer
+    tiles), branching and multi-root, verify and commit."""
+    cfg = cfg_of("gdn", batch=6, num_qk_heads=2, num_v_heads=4, d_k=128, d_v=128,
+                 prefix_len=0, max_nodes=128)
+    parents = [_multi_root(128, 1, 70), _multi_root(127, 3, 71),
+               W.topk_tree(np.random.default_rng([2, 72]), 120, (16, 4, 2), 12),
+               _multi_root(113, 2, 73), _multi_root(112, 1, 74), _multi_root(40, 2, 75)]
+    paths = [chain_path(p, int(np.argmax(W.node_depths(p)))) for p in parents]
+    w = custom(cfg, parents, paths, seed=128)
+    state = rand_state(cfg, len(parents), seed=12)
+    up = H.Uploaded(w)
+    print(f"delta rule dense kernel sizes={[len(p) for p in parents]}", flush=True)
+    got, err = H.run_verify(cfg, up, H.t_f32(state))
+    assert err == 0
+    assert H.slice_rel_err(got, o_verify(cfg, w, state), w.node_offsets) <= H.TOL
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st) == 0
+    assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
+
+
 @pytest.mark.parametrize("max_nodes, trees", [
     (176, [("roots", 176, 1), ("roots", 100, 2), ("roots", 17, 3), ("topk", 64, 0)]),
     (256, [("roots", 256, 1), ("roots", 177, 3), ("roots", 90, 2), ("roots", 15, 1), ("topk", 200, 0)]),
