@@ -28,11 +28,18 @@ namespace tl {
 
 constexpr int kCommitChunk = 32;   // path steps staged in LDS at a time
 
-template <int D>
+// A row of the stored state sits in LPR adjacent lanes, VPL values each, as
+// CH chunks of 4: chunk c of lane l holds columns 4 (l % LPR) + 4 LPR c, so
+// each load or store instruction covers whole 4 LPR-column runs of a row.
+// The delta rule sums every row once per path step; at d >= 64 its rows are
+// held by 8 lanes (three DPP steps per sum) instead of d / 4.
+template <int D, int MODE>
 struct CommitShape {
   static constexpr int ROWS = (D >= 64) ? 32 : D;   // state rows per streamed block
   static constexpr int NRB = D / ROWS;              // blocks per (request, v-head) slot
-  static constexpr int LPR = D / 4;                 // lanes per row (4 floats each)
+  static constexpr int VPL = (MODE == TL_MODE_GDN && D >= 64) ? D / 8 : 4;   // values per lane
+  static constexpr int LPR = D / VPL;               // lanes per row
+  static constexpr int CH = VPL / 4;                // 4-float chunks per lane and row
   static constexpr int RPP = kThreads / LPR;        // rows per pass of the workgroup
   static constexpr int PASSES = (ROWS + RPP - 1) / RPP;
 };
@@ -86,8 +93,9 @@ template <int MODE, int D, bool F32IN, bool TERMINAL, int SPLIT>
 __device__ __attribute__((always_inline)) inline void commit_unit(
     const CommitCommon& a, const CommitLayer& ly, const int32_t* path_offsets,
     const int32_t* path, const int32_t* terminal, int b, int h, int part) {
-  using SH = CommitShape<D>;
-  constexpr int ROWS = SH::ROWS, NRB = SH::NRB, LPR = SH::LPR, RPP = SH::RPP, PASSES = SH::PASSES;
+  using SH = CommitShape<D, MODE>;
+  constexpr int ROWS = SH::ROWS, NRB = SH::NRB, LPR = SH::LPR, CH = SH::CH, RPP = SH::RPP,
+                PASSES = SH::PASSES;
   static_assert(NRB % SPLIT == 0, "a slot splits into whole row blocks");
   constexpr int NB = NRB / SPLIT;   // row blocks of this workgroup
   const int rb0 = part * NB;
@@ -145,31 +153,39 @@ __device__ __attribute__((always_inline)) inline void commit_unit(
   // one straight-line sequence)
   const bool need = TERMINAL ? term >= 0 : Lp > 0;
   float* Sp = ly.state + ((size_t)sidx * a.Hv + h) * D * D;
-  const int col = (tid % LPR) * 4;
+  const int col = (tid % LPR) * 4;   // column of the lane's chunk 0; chunk c is 4 LPR c further
   const int rsub = tid / LPR;
   uint32_t keep = need ? 0xffffffffu : 0u;
   asm volatile("" : "+v"(keep));
-  auto load_block = [&](int rb, f32x4 (&st)[PASSES]) {
+  using Block = f32x4[PASSES][CH];
+  auto load_block = [&](int rb, Block& st) {
 #pragma unroll
     for (int p = 0; p < PASSES; ++p) {
       const int row = min(p * RPP + rsub, ROWS - 1);
-      const uint32_t o = (uint32_t)(((rb0 + rb) * ROWS + row) * D + col) & keep;
-      st[p] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(Sp + o));
+#pragma unroll
+      for (int c = 0; c < CH; ++c) {
+        const uint32_t o = (uint32_t)(((rb0 + rb) * ROWS + row) * D + col + 4 * LPR * c) & keep;
+        st[p][c] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(Sp + o));
+      }
     }
   };
-  auto store_block = [&](int rb, const f32x4 (&st)[PASSES]) {
+  auto store_block = [&](int rb, const Block& st) {
 #pragma unroll
     for (int p = 0; p < PASSES; ++p) {
       const int row = p * RPP + rsub;
-      if (row < ROWS)
-        __builtin_nontemporal_store(st[p], reinterpret_cast<f32x4*>(Sp + (size_t)((rb0 + rb) * ROWS + row) * D + col));
+      if (row < ROWS) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c)
+          __builtin_nontemporal_store(
+              st[p][c], reinterpret_cast<f32x4*>(Sp + (size_t)((rb0 + rb) * ROWS + row) * D + col + 4 * LPR * c));
+      }
     }
   };
   // gated linear attention keeps every block of the slot in registers (all
   // loads in flight at once); the delta rule needs more registers for its
   // row reductions and streams the blocks through two buffers
   constexpr int NBUF = GDN ? (NB < 2 ? NB : 2) : NB;
-  f32x4 sb[NBUF][PASSES];
+  Block sb[NBUF];
 #pragma unroll
   for (int rb = 0; rb < NBUF; ++rb) load_block(rb, sb[rb]);
 
@@ -219,49 +235,111 @@ __device__ __attribute__((always_inline)) inline void commit_unit(
     }
     __syncthreads();
   };
-  // replay staged steps [0, n) on the rows of block rb
-  auto replay = [&](int rb, int n, f32x4 (&st)[PASSES]) {
-    for (int t = 0; t < n; ++t) {
-      const float gam = s_gam[t];
-      const f32x4 kv = *reinterpret_cast<const f32x4*>(s_k + t * D + col);
+  // replay staged steps [0, n) on the rows of blocks rb .. rb + NR - 1, held
+  // in sb[i0 .. i0 + NR); the blocks share each step's k row
+  auto replay = [&](auto nr, int rb, int i0, int n) {
+    constexpr int NR = decltype(nr)::value;
+    if constexpr (!GDN) {
+      static_assert(CH == 1, "one chunk per lane and row");
+      for (int t = 0; t < n; ++t) {
+        const float gam = s_gam[t];
+        const f32x4 kv = *reinterpret_cast<const f32x4*>(s_k + t * D + col);
 #pragma unroll
-      for (int p = 0; p < PASSES; ++p) {
-        const int row = p * RPP + rsub;
-        const float vv = s_v[t * D + (rb0 + rb) * ROWS + (row < ROWS ? row : 0)];
-        if constexpr (!GDN) {
-          st[p] = gam * st[p] + vv * kv;
-        } else {
-          float part = st[p][0] * kv[0] + st[p][1] * kv[1] + st[p][2] * kv[2] + st[p][3] * kv[3];
-          part = group_sum<LPR>(part);   // the row's LPR lanes
-          const float u = s_beta[t] * (vv - gam * part);
-          st[p] = gam * st[p] + u * kv;
+        for (int i = 0; i < NR; ++i) {
+#pragma unroll
+          for (int p = 0; p < PASSES; ++p) {
+            const int row = p * RPP + rsub;
+            const float vv = s_v[t * D + (rb0 + rb + i) * ROWS + (row < ROWS ? row : 0)];
+            sb[i0 + i][p][0] = gam * sb[i0 + i][p][0] + vv * kv;
+          }
         }
       }
+    } else {
+      // The rows are held as S / scale, scale = the product of the decays
+      // so far, so that a step is one FMA per entry:
+      //   S~ += (u / scale) k^T,  u = beta (v - scale (S~ k)).
+      // When scale leaves [2^-32, 2^32] (or is not finite) it is folded into
+      // the rows and restarts at 1; the final scale is folded in before the
+      // rows are stored.  (Gated linear attention keeps gamma S + v k^T:
+      // there the folding measured slower, its replay having no sums.)
+      auto fold = [&](float f) {
+#pragma unroll
+        for (int i = 0; i < NR; ++i)
+#pragma unroll
+          for (int p = 0; p < PASSES; ++p)
+#pragma unroll
+            for (int c = 0; c < CH; ++c) sb[i0 + i][p][c] *= f;
+      };
+      float scale = 1.f;
+      for (int t = 0; t < n; ++t) {
+        scale *= s_gam[t];
+        if (!(scale >= 0x1p-32f && scale <= 0x1p32f)) {   // uniform
+          fold(scale);
+          scale = 1.f;
+        }
+        const float inv = __builtin_amdgcn_rcpf(scale);
+        const float bt = s_beta[t];
+        f32x4 kv[CH];
+#pragma unroll
+        for (int c = 0; c < CH; ++c) kv[c] = *reinterpret_cast<const f32x4*>(s_k + t * D + col + 4 * LPR * c);
+#pragma unroll
+        for (int i = 0; i < NR; ++i) {
+#pragma unroll
+          for (int p = 0; p < PASSES; ++p) {
+            f32x4* st = sb[i0 + i][p];
+            f32x4 acc = st[0] * kv[0];
+#pragma unroll
+            for (int c = 1; c < CH; ++c) acc += st[c] * kv[c];
+            float dot = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+            dot = group_sum<LPR>(dot);   // the row's LPR lanes
+            const int row = p * RPP + rsub;
+            const float vv = s_v[t * D + (rb0 + rb + i) * ROWS + (row < ROWS ? row : 0)];
+            const float cf = bt * (vv - scale * dot) * inv;
+#pragma unroll
+            for (int c = 0; c < CH; ++c) st[c] += cf * kv[c];
+          }
+        }
+      }
+      fold(scale);
     }
   };
+  using One = std::integral_constant<int, 1>;
+  using All = std::integral_constant<int, NB>;
 
   // with the whole slot in registers, the path rows are requested only once
   // the slot has arrived: scattered row reads issued into the middle of the
   // launch-wide state stream slowed it down
   if constexpr (NBUF == NB) wait_vmem();
-  if (Lp <= kCommitChunk) {
+  if constexpr (GDN && NBUF == NB) {
+    // every block is held: each chunk of steps is staged once and replayed
+    // on all of them
+    for (int c0 = 0; c0 < Lp; c0 += kCommitChunk) {
+      const int n = min(kCommitChunk, Lp - c0);
+      if (c0) __syncthreads();   // the previous chunk is fully consumed
+      stage(c0, n);
+      TL_TRACE_POINT(a, 4);
+      replay(All{}, 0, 0, n);
+    }
+#pragma unroll
+    for (int rb = 0; rb < NB; ++rb) store_block(rb, sb[rb]);
+  } else if (Lp <= kCommitChunk) {
     stage(0, Lp);
-    TL_TRACE_POINT(a, 4);
 #pragma unroll
     for (int rb = 0; rb < NB; ++rb) {
-      replay(rb, Lp, sb[rb % NBUF]);
+      replay(One{}, rb, rb % NBUF, Lp);
       store_block(rb, sb[rb % NBUF]);
       if (rb + NBUF < NB) load_block(rb + NBUF, sb[rb % NBUF]);
     }
   } else {
-    // long paths: the steps are staged chunk by chunk for every block
+    // long paths through streamed blocks: the steps are staged chunk by
+    // chunk for every block
 #pragma unroll
     for (int rb = 0; rb < NB; ++rb) {
       for (int c0 = 0; c0 < Lp; c0 += kCommitChunk) {
         const int n = min(kCommitChunk, Lp - c0);
         __syncthreads();   // the previous chunk is fully consumed
         stage(c0, n);
-        replay(rb, n, sb[rb % NBUF]);
+        replay(One{}, rb, rb % NBUF, n);
       }
       store_block(rb, sb[rb % NBUF]);
       if (rb + NBUF < NB) load_block(rb + NBUF, sb[rb % NBUF]);
@@ -348,7 +426,7 @@ template <int MODE, int D, bool F32IN>
 static tl_status launch_one(const CommitArgs& a, hipStream_t stream) {
   const long slots = (long)a.c.batch * a.c.Hv;
   if (slots == 0) return TL_OK;
-  constexpr int NRB = CommitShape<D>::NRB;
+  constexpr int NRB = CommitShape<D, MODE>::NRB;
   const long resident = resident_commit_blocks();
   if constexpr (NRB % 4 == 0) {
     if (resident > 0 && 2 * slots < resident) return launch_split<MODE, D, F32IN, 4>(a, slots, stream);
