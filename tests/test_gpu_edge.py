@@ -481,6 +481,37 @@ def test_tile_walk_gla_head_dims(d, max_nodes, sizes):
     assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
 
 
+@pytest.mark.parametrize("B", [3, 150, 260])
+def test_delta_rule_commit_decay_extremes(B):
+    """The delta-rule commit replays rows held as S divided by the running
+    decay product and folds that product back into them whenever it leaves
+    [2^-32, 2^32].  Three 45-step paths (two staging chunks) whose decays
+    force folds within and across chunks: decays down to e^-8 per step; a
+    zero decay (g = -inf) and an e^-50 one among decays of exactly one; and
+    growing decays (g = +0.5).  The other requests commit short paths, and
+    B (times 4 v-heads) puts the launch in each of its splits."""
+    cfg = cfg_of("gdn", batch=B, num_qk_heads=2, num_v_heads=4, prefix_len=0, max_nodes=64)
+    parents = [W.chain_tree(45)] * 3 + [W.chain_tree(3)] * (B - 3)
+    paths = [list(range(45))] * 3 + [list(range(1 + b % 3)) for b in range(B - 3)]
+    w = custom(cfg, parents, paths, seed=B)
+    rng = np.random.default_rng([B, 17])
+    g = w.g.copy()
+    g[0:45] = -8.0 * rng.random((45, 4))
+    g[45:90] = 0.0
+    g[45 + 20] = -np.inf
+    g[45 + 33] = -50.0
+    g[90:135] = 0.5
+    w = dataclasses.replace(w, g=g.astype(np.float32))
+    state = rand_state(cfg, B, seed=B)
+    up = H.Uploaded(w)
+    print(f"delta-rule commit decay extremes B={B} slots={4 * B}", flush=True)
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st) == 0
+    got = st.cpu().numpy()
+    assert np.isfinite(got).all()
+    assert H.state_rel_err(got, o_commit(cfg, w, state)) <= H.TOL
+
+
 @pytest.mark.parametrize("name", ["large", "gdn"])
 def test_deepest_tree_256_chain(name):
     cfg = cfg_of(name, batch=1, prefix_len=0, max_nodes=256)
