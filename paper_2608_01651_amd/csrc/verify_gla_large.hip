@@ -179,18 +179,26 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_wave
   // the wave's state rows last: the batch's wait leaves them in flight, and
   // they are first read after the topology
   f32x4 sraw[KS][2];
-  if (vw) {
+  auto load_state = [&]() __attribute__((always_inline)) {
     const float* row = a.state + ((size_t)sidx * a.Hv + h) * D * D + (size_t)(kTile * wave + lr) * D;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       sraw[ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 4 * lg));
       sraw[ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 16 + 4 * lg));
     }
-  }
+  };
+  // unconditional where every wave is a value wave, so that the compiler's
+  // count of outstanding loads is the same on every path and its waits for
+  // the parents and gates do not take in the state rows
+  if constexpr (VT == NW) load_state();
+  else if (vw) load_state();
   // ---- topology by wave 0: M+ rows, cl, per-tile OR of the M+ rows (rows
   // past T: zero masks and decays)
   int* s_flag = reinterpret_cast<int*>(tl_lds + L.flag);
   if (wave == 0) {   // uniform
+    // the parents and gates have landed; the state rows issued after them
+    // stay in flight through the topology
+    if constexpr (VT == NW) wait_vmem_below<2 * KS>();
     for (int x = lane; x < (tm / kTile) * W; x += 64) s_tmask[x] = 0;
     int* s_jmp = reinterpret_cast<int*>(s_frag);
     float* s_acc = reinterpret_cast<float*>(s_jmp + 64 * NE);
@@ -224,7 +232,8 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_wave
   TL_TRACE_POINT(a, 13);
   // batch 1 but the state rows has landed (loads complete in issue order; a
   // wait the compiler sees)
-  if (vw) wait_vmem_below<2 * KS>();
+  if constexpr (VT == NW) wait_vmem_below<2 * KS>();
+  else if (vw) wait_vmem_below<2 * KS>();
   else wait_vmem_below<0>();
   lds_barrier();          // staged V rows, Q rows and the topology are visible
   TL_TRACE_POINT(a, 2);
