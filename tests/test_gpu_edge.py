@@ -428,6 +428,40 @@ def test_delta_rule_dense_kernel_tile_counts():
     assert H.state_rel_err(st.cpu().numpy(), o_commit(cfg, w, state)) <= H.TOL
 
 
+@pytest.mark.parametrize("hk, hv, cap", [(4, 8, 128), (4, 16, 128), (8, 16, 64)])
+def test_delta_rule_dense_full_launch_ragged(hk, hv, cap):
+    """The dense delta-rule kernel at the size of the benchmark's launch
+    (B * Hv >= 2 x the GPU's compute units, so the grid runs in two rounds or
+    more): group sizes 2 and 4, node caps 128 and 64, ragged multi-root trees
+    of 1..cap nodes (full tiles among them), an empty request.  Every head of
+    sampled requests against the oracle, verify and commit."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    B = -(-2 * cus // hv) + 3
+    rng = np.random.default_rng([hk, hv, cap])
+    sizes = [cap, cap - 1, 0, 1, 15, 16, 17] + [int(x) for x in rng.integers(1, cap + 1, B - 7)]
+    parents = [_multi_root(T, 1 + b % 3, 900 + b) if T else np.zeros(0, np.int32)
+               for b, T in enumerate(sizes)]
+    paths = [chain_path(p, int(np.argmax(W.node_depths(p)))) if len(p) else [] for p in parents]
+    cfg = cfg_of("gdn", batch=B, num_qk_heads=hk, num_v_heads=hv, d_k=128, d_v=128,
+                 prefix_len=0, max_nodes=cap)
+    w = custom(cfg, parents, paths, seed=hv)
+    state = rand_state(cfg, B, seed=hk)
+    up = H.Uploaded(w)
+    keep = [0, 1, 3, 4, 5, 6, B // 2, B - 1]
+    print(f"delta rule dense full launch: Hk={hk} Hv={hv} cap={cap} B={B} slots={B * hv} cus={cus} "
+          f"sample={keep}", flush=True)
+    got, err = H.run_verify(cfg, up, H.t_f32(state))
+    assert err == 0
+    ws = sub(w, keep)
+    assert H.slice_rel_err(got[rows_of(w, keep)], o_verify(cfg, ws, state[keep]), ws.node_offsets) <= H.TOL
+    st = H.t_f32(state)
+    assert H.run_commit(cfg, up, st) == 0
+    got_s = st.cpu().numpy()
+    assert H.state_rel_err(got_s[keep], o_commit(cfg, ws, state[keep])) <= H.TOL
+    np.testing.assert_array_equal(got_s[2], state[2])   # the empty request's slot
+
+
 @pytest.mark.parametrize("max_nodes, trees", [
     (176, [("roots", 176, 1), ("roots", 100, 2), ("roots", 17, 3), ("topk", 64, 0)]),
     (256, [("roots", 256, 1), ("roots", 177, 3), ("roots", 90, 2), ("roots", 15, 1), ("topk", 200, 0)]),
