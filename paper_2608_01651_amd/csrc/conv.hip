@@ -36,11 +36,18 @@ namespace tl {
 
 static_assert(kConvCommitTile == kThreads * 8, "one 8-channel chunk per thread");
 
-// SiLU with the hardware exp2 and reciprocal (about 1 ulp each): the result
-// is stored as bf16, 2^-8 relative, so their error is far below it.  Large
-// negative y gives exp2 = inf and rcp = 0, i.e. -0.
-__device__ inline float silu(float y) {
-  return y * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-1.4426950408889634f * y));
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// log2(e) SiLU(y) from t = log2(e) y: t / (1 + 2^-t) = log2(e) y sigma(y).
+// The convolution forms t directly (weights and bias scaled by log2(e) once),
+// which saves a multiply per element; the factor log2(e) then cancels in the
+// q/k normalisation (with eps scaled by log2(e)^2) and is taken out of v by
+// the output scale.  Hardware exp2 and reciprocal (about 1 ulp each): the
+// result is stored as bf16, 2^-8 relative, so their error is far below it.
+// Large negative t gives exp2 = inf and rcp = 0, i.e. -0.
+__device__ inline float silu_log2e(float t) {
+  return t * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-t));
 }
 __device__ inline float softplus(float x) { return fmaxf(x, 0.f) + log1pf(expf(-fabsf(x))); }
 __device__ inline float sigmoidf(float x) { return 1.f / (1.f + expf(-x)); }
@@ -71,8 +78,8 @@ __global__ __launch_bounds__(kThreads) void conv_gates_kernel(ConvArgs a) {
 #pragma unroll
     for (int t = 0; t < 2 * WIDTH; ++t) wr[t] = wv[t];
   }
-  const f32x4 b0 = *reinterpret_cast<const f32x4*>(a.conv_bias + cc);
-  const f32x4 b1 = *reinterpret_cast<const f32x4*>(a.conv_bias + cc + 4);
+  f32x4 b0 = *reinterpret_cast<const f32x4*>(a.conv_bias + cc);
+  f32x4 b1 = *reinterpret_cast<const f32x4*>(a.conv_bias + cc + 4);
 
   Request rq;
   if (!load_request(a.node_offsets, b, a.max_nodes, a.dev_err, rq)) return;
@@ -146,30 +153,31 @@ __global__ __launch_bounds__(kThreads) void conv_gates_kernel(ConvArgs a) {
     dst_row = (size_t)a.Hv * a.dv;
   }
   const int lo = (lane % LPN) * 16;   // the lane's byte offset in a tile row
+#pragma unroll
+  for (int t = 0; t < 2 * WIDTH; ++t) wr[t] *= kLog2e;   // the convolution forms log2(e) y
+  b0 *= kLog2e;
+  b1 *= kLog2e;
   TL_TRACE_POINT(a, 2);
 
   for (int base = 0; base < T; base += kWaves * NPW) {
     const int n = base + wave * NPW + lane / LPN;
     const int nc = n < T ? n : T - 1;   // lanes past T compute a valid node and store nothing
     // window position WIDTH - 1 - s: the node s steps up, or, once the root
-    // is passed after L nodes, state row WIDTH - 2 - (s - L)
+    // is passed, the committed state rows newest first.  j < 0 stands for
+    // state row WIDTH - 1 + j, so a step is j <- parent(j) for a node and
+    // j <- j - 1 past the root; the row is picked by a select, without
+    // branches (lanes walk different paths)
     bf16x8 win[WIDTH];
-    win[WIDTH - 1] = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(s_x) + nc * RB + lo);
-    int j = nc, L = 0;
+    const char* xb = reinterpret_cast<const char*>(s_x) + lo;
+    const char* cb = reinterpret_cast<const char*>(s_cs) + lo;
+    win[WIDTH - 1] = *reinterpret_cast<const bf16x8*>(xb + nc * RB);
+    int j = nc;
 #pragma unroll
     for (int s = 1; s < WIDTH; ++s) {
-      const int p = WIDTH - 1 - s;
-      if (L == 0) {
-        const int pj = s_par[j];
-        if (pj >= 0) {
-          win[p] = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(s_x) + pj * RB + lo);
-          j = pj;
-          continue;
-        }
-        L = s;
-      }
-      win[p] = *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(s_cs) +
-                                                (WIDTH - 2 - (s - L)) * RB + lo);
+      const int pj = s_par[j > 0 ? j : 0];
+      j = j >= 0 ? pj : j - 1;
+      const char* row = j >= 0 ? xb + j * RB : cb + (WIDTH - 1 + j) * RB;
+      win[WIDTH - 1 - s] = *reinterpret_cast<const bf16x8*>(row);
     }
     float z[8];
 #pragma unroll
@@ -180,7 +188,7 @@ __global__ __launch_bounds__(kThreads) void conv_gates_kernel(ConvArgs a) {
         const int f = e * WIDTH + p;   // W[c0 + e, p]
         y += wr[f >> 2][f & 3] * (float)win[p][e];
       }
-      z[e] = silu(y);
+      z[e] = silu_log2e(y);   // log2(e) SiLU(y)
     }
     // per-head normalisation of q and k: a head's d_k channels are d_k / 8
     // adjacent lanes of one node's lane group
@@ -193,7 +201,7 @@ __global__ __launch_bounds__(kThreads) void conv_gates_kernel(ConvArgs a) {
       case 64: ss = group_sum<8>(ss); break;
       default: ss = group_sum<16>(ss); break;
     }
-    const float scale = norm ? rsqrtf(ss + a.eps) : 1.f;
+    const float scale = norm ? rsqrtf(ss + a.eps * (kLog2e * kLog2e)) : kLn2;
     if (live && n < T) {
       bf16x8 out;
 #pragma unroll
