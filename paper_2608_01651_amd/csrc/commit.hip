@@ -112,21 +112,25 @@ __device__ __attribute__((always_inline)) inline void commit_unit(
   TL_TRACE_POINT(a, 0);
   const int hq = h / (a.Hv / a.Hk);
 
-  Request rq;
-  if (!load_request(a.node_offsets, b, a.max_nodes, a.dev_err, rq)) return;
-  const int T = rq.T, off = rq.off;
+  // the request's path descriptor and slot are requested together with its
+  // node range (independent loads: one round trip, not three)
   int p0 = 0, Lp = 0, term = -1;
   if constexpr (TERMINAL) {
     term = terminal[b];
   } else {
     p0 = path_offsets[b];
     Lp = path_offsets[b + 1] - p0;
+  }
+  const int sidx = a.slot ? a.slot[b] : b;
+  Request rq;
+  if (!load_request(a.node_offsets, b, a.max_nodes, a.dev_err, rq)) return;
+  const int T = rq.T, off = rq.off;
+  if constexpr (!TERMINAL) {
     if (p0 < 0 || Lp < 0) {
       if (tid == 0) report(a.dev_err, TL_EINVAL);
       return;
     }
   }
-  const int sidx = a.slot ? a.slot[b] : b;
   if (sidx < 0 || sidx >= a.num_slots) {
     if (tid == 0) report(a.dev_err, TL_EINVAL);
     return;
@@ -363,8 +367,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     CommitLayersArgsN<NL> a) {
   const int per_layer = a.c.batch * a.c.Hv;
   const int layer = blockIdx.x / per_layer, rem = blockIdx.x % per_layer;
-  commit_unit<MODE, D, F32IN, true, 1>(a.c, a.ly[layer], nullptr, nullptr, a.terminal, rem / a.c.Hv,
-                                       rem % a.c.Hv, 0);
+  // a launch of one layer indexes its table statically, so that the kernel
+  // arguments are read in a few wide loads at the start
+  commit_unit<MODE, D, F32IN, true, 1>(a.c, a.ly[NL == 1 ? 0 : layer], nullptr, nullptr, a.terminal,
+                                       rem / a.c.Hv, rem % a.c.Hv, 0);
 }
 
 // Accepted path of every request from its terminal node: path_len[b] and the
