@@ -81,11 +81,12 @@ __global__ __launch_bounds__(kThreads) void conv_gates_kernel(ConvArgs a) {
   f32x4 b0 = *reinterpret_cast<const f32x4*>(a.conv_bias + cc);
   f32x4 b1 = *reinterpret_cast<const f32x4*>(a.conv_bias + cc + 4);
 
+  // the slot is read with the node range (independent loads, one round trip)
+  const int sidx = a.slot ? a.slot[b] : b;
   Request rq;
   if (!load_request(a.node_offsets, b, a.max_nodes, a.dev_err, rq)) return;
   const int T = rq.T;
   if (T == 0) return;
-  const int sidx = a.slot ? a.slot[b] : b;
   if (sidx < 0 || sidx >= a.num_slots) {
     if (tid == 0) report(a.dev_err, TL_EINVAL);
     return;
@@ -228,10 +229,13 @@ __global__ __launch_bounds__(kThreads) void conv_state_commit_kernel(ConvCommitA
   __shared__ int s_par[kMaxNodes];
   const int tile = blockIdx.x % a.tiles, b = blockIdx.x / a.tiles;
   const int tid = threadIdx.x;
+  // the terminal node and the slot are read with the node range (independent
+  // loads, one round trip)
+  const int term = a.terminal[b];
+  const int sidx = a.slot ? a.slot[b] : b;
   Request rq;
   if (!load_request(a.node_offsets, b, a.max_nodes, a.dev_err, rq)) return;
-  const int T = rq.T, term = a.terminal[b];
-  const int sidx = a.slot ? a.slot[b] : b;
+  const int T = rq.T;
   if (sidx < 0 || sidx >= a.num_slots) {
     if (tid == 0) report(a.dev_err, TL_EINVAL);
     return;

@@ -79,12 +79,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NH == 
   u.slice = w_in % NSL;
   u.tm = a.tm;
 
+  // the slot is read with the node range (independent loads, one round trip)
+  u.sidx = a.slot ? a.slot[u.b] : u.b;
   Request rq;
   if (!load_request(a.node_offsets, u.b, a.max_nodes, a.dev_err, rq)) return;
   u.off = rq.off;
   u.T = rq.T;
   if (u.T == 0) return;
-  u.sidx = a.slot ? a.slot[u.b] : u.b;
   if (u.sidx < 0 || u.sidx >= a.num_slots) {
     if (tid == 0) report(a.dev_err, TL_EINVAL);
     return;

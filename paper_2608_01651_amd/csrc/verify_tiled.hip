@@ -103,11 +103,12 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
   const int sh = (local / grp) * 8 + xcd;
   if (sh >= nshare) return;
   const int b = sh / a.Hk, hq = sh % a.Hk, h = hq * grp + local % grp;
+  // the slot is read with the node range (independent loads, one round trip)
+  const int sidx = a.slot ? a.slot[b] : b;
   Request rq;
   if (!load_request(a.node_offsets, b, a.max_nodes, a.dev_err, rq)) return;
   const int T = rq.T, off = rq.off;
   if (T == 0) return;
-  const int sidx = a.slot ? a.slot[b] : b;
   if (sidx < 0 || sidx >= a.num_slots) {
     if (tid == 0) report(a.dev_err, TL_EINVAL);
     return;

@@ -177,8 +177,17 @@ def test_tree_larger_than_max_nodes_is_reported():
     assert np.isnan(got).all()
 
 
-def test_slot_out_of_range_is_reported():
-    cfg, parents, paths = _error_case("production", {})
+# every verify kernel reads the slot map: (config, node cap, tree size)
+SLOT_KERNELS = [("production", 64, 64),     # small-tree kernel
+                ("gdn", 128, 100),          # dense delta-rule kernel
+                ("large", 256, 200),        # large-tree kernel
+                ("gdn", 144, 140),          # the delta rule tile by tile
+                ("gdn", 256, 180)]          # the delta rule's per-wave path
+
+
+@pytest.mark.parametrize("name, cap, T", SLOT_KERNELS)
+def test_slot_out_of_range_is_reported(name, cap, T):
+    cfg, parents, paths = _error_case(name, dict(max_nodes=cap), T=T)
     w = custom(cfg, parents, paths)
     state = rand_state(cfg, 4)
     slot = H.t_int([2, 4, 0])            # 4 is past the last of the 4 slots
@@ -214,9 +223,10 @@ def test_empty_paths_and_empty_requests(name):
     assert H.state_rel_err(after, o_commit(cfg, w, state)) <= H.TOL
 
 
-def test_slot_indirection():
-    cfg = cfg_of("production", batch=3, prefix_len=0)
-    parents = [topk(64, s) for s in range(3)]
+@pytest.mark.parametrize("name, cap, T", SLOT_KERNELS)
+def test_slot_indirection(name, cap, T):
+    cfg = cfg_of(name, batch=3, prefix_len=0, max_nodes=cap)
+    parents = [topk(T, s) for s in range(3)]
     paths = [chain_path(p, 20) for p in parents]
     w = custom(cfg, parents, paths)
     state = rand_state(cfg, 5)
