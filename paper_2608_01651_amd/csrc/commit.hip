@@ -360,17 +360,28 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
                                             slot % a.c.Hv, part);
 }
 
-// One workgroup per (layer, request, v-head) slot; consecutive workgroups
-// walk the v-heads, then the requests, then the layers.
+// Workgroups per slot in the unified commit: the delta rule's slots go to two
+// (each holds its two row blocks and replays them side by side, as the
+// single-layer commit does below its slot count threshold).
+template <int MODE, int D>
+constexpr int layers_split() {
+  return (MODE == TL_MODE_GDN && CommitShape<D, MODE>::NRB % 2 == 0) ? 2 : 1;
+}
+
+// layers_split() workgroups per (layer, request, v-head) slot; consecutive
+// workgroups walk the slot's parts, the v-heads, then the requests, then the
+// layers.
 template <int MODE, int D, bool F32IN, int NL>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void commit_layers_kernel(
     CommitLayersArgsN<NL> a) {
-  const int per_layer = a.c.batch * a.c.Hv;
+  constexpr int SPLIT = layers_split<MODE, D>();
+  const int per_layer = a.c.batch * a.c.Hv * SPLIT;
   const int layer = blockIdx.x / per_layer, rem = blockIdx.x % per_layer;
+  const int slot = rem / SPLIT, part = rem % SPLIT;
   // a launch of one layer indexes its table statically, so that the kernel
   // arguments are read in a few wide loads at the start
-  commit_unit<MODE, D, F32IN, true, 1>(a.c, a.ly[NL == 1 ? 0 : layer], nullptr, nullptr, a.terminal,
-                                       rem / a.c.Hv, rem % a.c.Hv, 0);
+  commit_unit<MODE, D, F32IN, true, SPLIT>(a.c, a.ly[NL == 1 ? 0 : layer], nullptr, nullptr, a.terminal,
+                                           slot / a.c.Hv, slot % a.c.Hv, part);
 }
 
 // Accepted path of every request from its terminal node: path_len[b] and the
@@ -445,7 +456,7 @@ static tl_status launch_one(const CommitArgs& a, hipStream_t stream) {
 
 template <int MODE, int D, bool F32IN, int NL>
 static tl_status launch_one(const CommitLayersArgsN<NL>& a, hipStream_t stream) {
-  const long blocks = (long)a.num_layers * a.c.batch * a.c.Hv;
+  const long blocks = (long)a.num_layers * a.c.batch * a.c.Hv * layers_split<MODE, D>();
   if (blocks == 0) return TL_OK;
   if (blocks > 0x7fffffffL) return TL_EINVAL;
   hipLaunchKernelGGL((commit_layers_kernel<MODE, D, F32IN, NL>), dim3((unsigned)blocks), dim3(kThreads),
