@@ -224,14 +224,16 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   }
   TL_TRACE_POINT(a, 6);
   // S^T as the B operand of 16x16x32 products: column = channel 16 wave + lr
-  // (a row of the stored slot), K = the key channels of chunk ks in kpos order
+  // (a row of the stored slot), K = key channels 32 ks + 8 lg .. + 7 of chunk
+  // ks for lane group lg (the products over d_k take K in this order, so a K
+  // or Q operand is one 16-byte chunk of a staged row)
   f32x4 sraw[KS][2];
   {
     const float* row = a.state + ((size_t)sidx * a.Hv + h) * D * D + (size_t)(kTile * wave + lr) * D;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      sraw[ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 4 * lg));
-      sraw[ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 16 + 4 * lg));
+      sraw[ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 8 * lg));
+      sraw[ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 8 * lg + 4));
     }
   }
 
@@ -296,14 +298,14 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   lds_barrier();   // every wave has read the staged V rows (the C blocks go over them)
   TL_TRACE_POINT(a, 3);
 
-  // operand fragment of row R + lr of the swizzled K or Q rows (R a multiple of 16)
+  // operand fragment of row R + lr of the swizzled K or Q rows (R a multiple
+  // of 16): key channels 32 ks + 8 lg .. + 7, i.e. 16-byte chunk 4 ks + lg of
+  // the row, one read (the swizzle puts the 16 rows' chunks on distinct banks)
   const int key = lr & (CPRK - 1);
-  const int fo_row = lr * D * 2 + (lg & 1) * 8;
+  const int fo_row = lr * D * 2;
   auto frag = [&](const __bf16* base, int R, int ks) __attribute__((always_inline)) {
     const unsigned char* p = reinterpret_cast<const unsigned char*>(base) + R * D * 2 + fo_row;
-    const bf16x4 x0 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + (lg >> 1)) ^ key) * 16));
-    const bf16x4 x1 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + 2 + (lg >> 1)) ^ key) * 16));
-    return bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+    return *reinterpret_cast<const bf16x8*>(p + (((4 * ks + lg) ^ key) * 16));
   };
   // block x (fp32, MFMA fragment layout) into half `half` of pair `pair`
   auto put_half = [&](unsigned char* base, int pair, int half, const f32x4& x) __attribute__((always_inline)) {
