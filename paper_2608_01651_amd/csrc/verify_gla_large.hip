@@ -184,8 +184,8 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_wave
     const float* row = a.state + ((size_t)sidx * a.Hv + h) * D * D + (size_t)(kTile * wave + lr) * D;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      sraw[ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 4 * lg));
-      sraw[ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 16 + 4 * lg));
+      sraw[ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 8 * lg));
+      sraw[ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 8 * lg + 4));
     }
   };
   // unconditional where every wave is a value wave, so that the compiler's
@@ -300,12 +300,10 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_wave
   // operand fragment of row R + lr (R a multiple of 16), K chunk ks, of a
   // swizzled LDS matrix
   const int key = lr & (CPRK - 1);
-  const int fo_row = lr * D * 2 + (lg & 1) * 8;
+  const int fo_row = lr * D * 2;
   auto frag = [&](const __bf16* base, int R, int ks) __attribute__((always_inline)) {
     const unsigned char* p = reinterpret_cast<const unsigned char*>(base) + R * D * 2 + fo_row;
-    const bf16x4 x0 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + (lg >> 1)) ^ key) * 16));
-    const bf16x4 x1 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + 2 + (lg >> 1)) ^ key) * 16));
-    return bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+    return *reinterpret_cast<const bf16x8*>(p + (((4 * ks + lg) ^ key) * 16));
   };
   // the tile masks, word x in lane x (at most 64 words), and 32 bits of tile
   // I's mask starting at node 32 c, read across lanes (uniform)

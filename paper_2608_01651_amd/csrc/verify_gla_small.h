@@ -146,8 +146,8 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
       const float* row = Sp + (size_t)(kTile * mtile(m) + lr) * D;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        sraw[hh][m][ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 4 * lg));
-        sraw[hh][m][ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 16 + 4 * lg));
+        sraw[hh][m][ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 8 * lg));
+        sraw[hh][m][ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 8 * lg + 4));
       }
     }
     issue_fence();
@@ -241,12 +241,10 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
   // operand fragment of row R + lr (R a multiple of 16), K chunk ks, from a
   // swizzled LDS matrix (fixed per-lane offsets inside a 16-row block)
   const int key = lr & (CPRK - 1);
-  const int fo_row = lr * D * 2 + (lg & 1) * 8;
+  const int fo_row = lr * D * 2;
   auto frag_at = [&](const __bf16* base, int R, int ks) {
     const unsigned char* p = reinterpret_cast<const unsigned char*>(base) + R * D * 2 + fo_row;
-    const bf16x4 x0 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + (lg >> 1)) ^ key) * 16));
-    const bf16x4 x1 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + 2 + (lg >> 1)) ^ key) * 16));
-    return bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+    return *reinterpret_cast<const bf16x8*>(p + (((4 * ks + lg) ^ key) * 16));
   };
 
   // per-node values of the four node tiles, read once: M+ rows (zero for

@@ -146,8 +146,8 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     const float* row = a.state + ((size_t)sidx * a.Hv + h) * D * D + (size_t)(kTile * wave + lr) * D;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      sraw[ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 4 * lg));
-      sraw[ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 16 + 4 * lg));
+      sraw[ks][0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 8 * lg));
+      sraw[ks][1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + ks * 32 + 8 * lg + 4));
     }
   }
   for (int base = wave * 64; base < T * CPRK; base += NT) {
@@ -215,13 +215,11 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
 
   // operand fragment of row R + lr of the swizzled K rows (R a multiple of 16)
   const int key = lr & (CPRK - 1);
-  const int fo_row = lr * D * 2 + (lg & 1) * 8;
+  const int fo_row = lr * D * 2;
   const unsigned char* kbase = reinterpret_cast<const unsigned char*>(s_k);
   auto kfrag = [&](int R, int ks) {
     const unsigned char* p = kbase + R * D * 2 + fo_row;
-    const bf16x4 x0 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + (lg >> 1)) ^ key) * 16));
-    const bf16x4 x1 = *reinterpret_cast<const bf16x4*>(p + (((4 * ks + 2 + (lg >> 1)) ^ key) * 16));
-    return bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+    return *reinterpret_cast<const bf16x8*>(p + (((4 * ks + lg) ^ key) * 16));
   };
   // A-operand fragment of U^T row (16 w + lr), node chunk c
   const int uo = ((kTile * wave + lr) * TS + 4 * lg) * 2;
@@ -246,9 +244,7 @@ __global__ __launch_bounds__(64 * tiled_waves(D)) void verify_tiled_kernel(Verif
     const __bf16* row = Qb + (size_t)r * qk_row;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const bf16x4 x0 = *reinterpret_cast<const bf16x4*>(row + ks * 32 + 4 * lg);
-      const bf16x4 x1 = *reinterpret_cast<const bf16x4*>(row + ks * 32 + 16 + 4 * lg);
-      dst[ks] = bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+      dst[ks] = *reinterpret_cast<const bf16x8*>(row + ks * 32 + 8 * lg);
     }
   };
   auto load_v = [&](int I) {
