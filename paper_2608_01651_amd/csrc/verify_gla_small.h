@@ -139,6 +139,7 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
   static_assert(FULL || MT == 1, "a wave owns all of its MT value tiles or none");
   auto load_state = [&](int hh) {
     issue_fence();
+    __builtin_amdgcn_s_setprio(0);
     const float* Sp = a.state + ((size_t)u.sidx * a.Hv + h0 + hh) * D * D + (size_t)slice * BV * D;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
@@ -159,7 +160,13 @@ __device__ inline void verify_gla_small(const VerifyArgs& a, const Unit u) {
     if (FULL || has_tile(0)) wait_vmem_below<NSL>();
     else wait_vmem();
   };
-  // ---- prologue: loads, and the topology on wave 0
+  // ---- prologue: loads, and the topology on wave 0.  Two workgroups share
+  // a CU, and the older one's waves win the issue arbitration; the waves
+  // issue their parents, gates and copies at raised priority and their state
+  // rows at the normal one, so that both workgroups' copies enter the CU's
+  // memory queue ahead of either's state rows and both can start on the
+  // coefficients while the state streams in.
+  __builtin_amdgcn_s_setprio(2);
   TL_TRACE_POINT(a, 1);
   int par = -1;
   float gx[NH];
