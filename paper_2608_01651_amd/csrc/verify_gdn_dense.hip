@@ -188,6 +188,11 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   // inline assembly, which the compiler does not count, and loads complete
   // in issue order.
   TL_TRACE_POINT(a, 1);
+  // The parents, gates and copies are issued at raised wave priority and the
+  // state rows at the normal one, so that every wave's copies reach the
+  // memory queue before any wave's state rows (the older waves would
+  // otherwise win the issue arbitration with their state loads).
+  __builtin_amdgcn_s_setprio(2);
   constexpr int NE = W;   // nodes per lane of wave 0 (node cap <= 64 W)
   int par[NE];
   float gx[NE], bx[NE];
@@ -228,6 +233,7 @@ __global__ __launch_bounds__(kDenseThreads) __attribute__((amdgpu_waves_per_eu(2
   // ks for lane group lg (the products over d_k take K in this order, so a K
   // or Q operand is one 16-byte chunk of a staged row)
   f32x4 sraw[KS][2];
+  __builtin_amdgcn_s_setprio(0);
   {
     const float* row = a.state + ((size_t)sidx * a.Hv + h) * D * D + (size_t)(kTile * wave + lr) * D;
 #pragma unroll

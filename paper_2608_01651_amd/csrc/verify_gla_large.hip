@@ -149,6 +149,11 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_wave
   // assembly, which the compiler does not count, so wave 0, whose waits the
   // compiler places, issues none.
   TL_TRACE_POINT(a, 1);
+  // The parents, gates and copies are issued at raised wave priority and the
+  // state rows at the normal one, so that every wave's copies reach the
+  // memory queue before any wave's state rows (the older waves would
+  // otherwise win the issue arbitration with their state loads).
+  __builtin_amdgcn_s_setprio(2);
   int par[NE];
   float gx[NE];
   if (wave == 0) {   // uniform
@@ -191,6 +196,7 @@ __global__ __launch_bounds__(64 * gla_large_waves(D)) __attribute__((amdgpu_wave
   // unconditional where every wave is a value wave, so that the compiler's
   // count of outstanding loads is the same on every path and its waits for
   // the parents and gates do not take in the state rows
+  __builtin_amdgcn_s_setprio(0);   // the state rows at the normal priority
   if constexpr (VT == NW) load_state();
   else if (vw) load_state();
   // ---- topology by wave 0: M+ rows, cl, per-tile OR of the M+ rows (rows
